@@ -1,0 +1,203 @@
+#!/usr/bin/env python3
+"""Throughput of the SSDi8 INT8 SSD chunk scan (one SSD layer) on one MI355X.
+
+A step is one whole layer on one batch of synthetic Mamba-2-shaped input already resident in
+HBM: quantize B and C per group (ssdi8_quantize_act x 2) and ssdi8_ssd_chunk_scan (ChunkBMM,
+ChunkCumsum + ChunkState, StatePassing, ChunkScan 1+2 with the D skip and the correction).
+Scales are static (calibrated offline by the CPU oracle; stored in tests/golden/calib).
+
+Prints ONE JSON line: tokens/s per layer, ms/step, the roofline of the dominant kernel measured
+live with HIP events on the launch stream, per-module times, and the CPU oracle timed on a
+bounded sample of the same workload on this host's cores.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0           # MI355X HBM3E, published
+MODULES = ("chunk_bmm", "chunk_state", "state_pass", "chunk_scan")
+
+
+def algorithmic_bytes(cfg):
+    """Minimum HBM bytes each kernel must move for its inputs and outputs (per launch)."""
+    B, L, H, P, G, N, Q = (cfg.batch, cfg.seqlen, cfg.nheads, cfg.headdim, cfg.ngroups,
+                           cfg.dstate, cfg.chunk)
+    T, c = B * L, L // Q
+    sx = 2 if cfg.dtype == "fp16" else 4
+    states = B * c * H * P * N                       # one int8 state tensor (B,c,H,P,N)
+    cb_causal = B * c * G * Q * (Q + 1) // 2
+    return {
+        "quantize_B": T * G * N * (sx + 1),
+        "quantize_C": T * G * N * (sx + 1),
+        "chunk_bmm": 2 * T * G * N + cb_causal,
+        "chunk_state": T * H * P * sx + T * H * 4 + T * G * N + states + B * H * c * 2,
+        "state_pass": 2 * states + B * H * c * 2 + B * H * P * N * 5,
+        "chunk_scan": 2 * T * H * P * sx + T * H * 4 + T * G * N + states + cb_causal,
+    }
+
+
+def layer_min_bytes(cfg):
+    """Layer-level minimum: x, dt, B, C in; y and the final state out."""
+    B, L, H, P, G, N = cfg.batch, cfg.seqlen, cfg.nheads, cfg.headdim, cfg.ngroups, cfg.dstate
+    sx = 2 if cfg.dtype == "fp16" else 4
+    T = B * L
+    return 2 * T * H * P * sx + T * H * 4 + 2 * T * G * N * sx + B * H * P * N * 5
+
+
+def cpu_baseline(cfg, inp, sc, budget_s: float):
+    """The CPU oracle as it stands, timed on a bounded sample: batch element 0, the first
+    `nh` heads (all chunks), nh sized from a one-head pilot to about `budget_s` seconds."""
+    import numpy as np
+    import threadpoolctl
+    from oracle import int8
+
+    def run(nh):
+        t = time.perf_counter()
+        int8.ssdi8_forward(inp["x"][:1, :, :nh], inp["dt_raw"][:1, :, :nh], inp["A"][:nh],
+                           inp["B"][:1], inp["C"][:1], inp["D"][:nh], sc["corr"][:nh],
+                           {"alpha_B": sc["alpha_B"], "alpha_C": sc["alpha_C"],
+                            "alpha_Xs": sc["alpha_Xs"][:nh], "alpha_S": sc["alpha_S"][:nh],
+                            "alpha_CB": sc["alpha_CB"]},
+                           chunk=cfg.chunk, want=("y",))
+        return time.perf_counter() - t
+
+    G = cfg.ngroups
+    hpg = cfg.nheads // G
+    pilot = run(1)
+    nh = int(max(1, min(cfg.nheads, budget_s / max(pilot, 1e-3))))
+    if G > 1:
+        nh = min(nh, hpg)                     # stay inside group 0 (its B, C were sliced)
+    t = run(nh)
+    info = threadpoolctl.threadpool_info()
+    threads = max([i.get("num_threads", 1) for i in info] or [1])
+    tokens = cfg.seqlen * nh / cfg.nheads     # layer-tokens: a token carries all H heads
+    return {"value": tokens / t, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"batch element 0, heads 0..{nh - 1} of {cfg.nheads}, {cfg.seqlen} "
+                      f"tokens ({t:.1f} s; tokens/s counted as layer tokens = "
+                      f"token-heads / {cfg.nheads})",
+            "seconds": round(t, 2), "host_cpus": len(os.sched_getaffinity(0))}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="mamba2-130m")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget-s", type=float, default=15.0)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: --gpus {args.gpus} is not supported by this build "
+              "(the SSD path shards over batch/heads with no exchange; see DESIGN.md).",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2608_21952_amd import ssdi8, synth
+
+    cfg = synth.CONFIGS[args.workload]
+    calib = os.path.join(ROOT, "tests", "golden", "calib", cfg.name + ".npz")
+    with np.load(calib, allow_pickle=False) as z:
+        sc = {k: z[k] for k in z.files}
+    print(f"[bench] workload {cfg.name}: B={cfg.batch} L={cfg.seqlen} H={cfg.nheads} "
+          f"P={cfg.headdim} N={cfg.dstate} G={cfg.ngroups} Q={cfg.chunk} {cfg.dtype}",
+          file=sys.stderr, flush=True)
+    inp = synth.draw(cfg, 1)
+    torch.cuda.set_device(0)
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    f32 = lambda a: dev(np.asarray(a, np.float32))
+    x, dt, Bf, Cf = dev(inp["x"]), dev(inp["dt_raw"]), dev(inp["B"]), dev(inp["C"])
+    A, D, corr = f32(inp["A"]), f32(inp["D"]), f32(sc["corr"])
+    aB, aC, aXs, aS, aCB = (f32(sc[k]) for k in ("alpha_B", "alpha_C", "alpha_Xs", "alpha_S",
+                                                 "alpha_CB"))
+    Bq = torch.empty(Bf.shape, dtype=torch.int8, device="cuda")
+    Cq = torch.empty(Cf.shape, dtype=torch.int8, device="cuda")
+    y = torch.empty_like(x)
+    ws = torch.empty(ssdi8.workspace_size(ssdi8.dims(cfg.batch, cfg.seqlen, cfg.nheads,
+                                                     cfg.ngroups)), dtype=torch.uint8,
+                     device="cuda")
+    K, W = args.steps, args.warmup
+    ev = ssdi8.HipEvents(7 * max(K, 1))
+
+    def step(k=None):
+        if k is not None:
+            ev.record(7 * k)
+        ssdi8.quantize_act(Bf, "group", aB, out=Bq)
+        if k is not None:
+            ev.record(7 * k + 1)
+        ssdi8.quantize_act(Cf, "group", aC, out=Cq)
+        ssdi8.ssd_chunk_scan(x, dt, A, Bq, Cq, aB, aC, aXs, aS, aCB, D=D, corr=corr,
+                             workspace=ws, y=y, final_state=True,
+                             stage_events=None if k is None else ev.group(7 * k + 2))
+
+    for _ in range(W):
+        step()
+    torch.cuda.synchronize()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for k in range(K):
+        step(k)
+    t1.record()
+    torch.cuda.synchronize()
+    total_ms = t0.elapsed_time(t1)
+    ms_step = total_ms / K
+    # per-module averages over the timed steps (events on the launch stream)
+    names = ("quantize_B", "quantize_C") + MODULES
+    per = {n: 0.0 for n in names}
+    for k in range(K):
+        base = 7 * k
+        per["quantize_B"] += ev.elapsed_ms(base, base + 1)
+        per["quantize_C"] += ev.elapsed_ms(base + 1, base + 2)
+        for i, n in enumerate(MODULES):
+            per[n] += ev.elapsed_ms(base + 2 + i, base + 3 + i)
+    per = {n: v / K for n, v in per.items()}
+    ev.close()
+    abytes = algorithmic_bytes(cfg)
+    stages = {n: {"us": round(per[n] * 1e3, 2),
+                  "GBps": round(abytes[n] / (per[n] * 1e-3) / 1e9, 1),
+                  "hbm_frac": round(abytes[n] / (per[n] * 1e-3) / 1e9 / HBM_PEAK_GBS, 3)}
+              for n in names}
+    dom = "chunk_scan"
+    ach = abytes[dom] / (per[dom] * 1e-3) / 1e9
+    tokens = cfg.batch * cfg.seqlen
+    value = tokens / (ms_step * 1e-3)
+    traffic_path = os.path.join(ROOT, "profiles", f"traffic_{dom}_{cfg.name}.json")
+    traffic = None
+    if os.path.exists(traffic_path):
+        with open(traffic_path) as f:
+            traffic = json.load(f).get("bytes_per_launch")
+    result = {
+        "metric": "INT8 SSD chunk-scan tokens/s per layer",
+        "value": value, "unit": "tokens/s", "n_gpus": 1, "steps": K, "warmup": W,
+        "ms_per_step": ms_step, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "int8+fp16", "data": "synthetic",
+        "config": {"workload": cfg.name, "batch": cfg.batch, "seqlen": cfg.seqlen,
+                   "nheads": cfg.nheads, "headdim": cfg.headdim, "dstate": cfg.dstate,
+                   "ngroups": cfg.ngroups, "chunk": cfg.chunk, "io_dtype": cfg.dtype},
+        "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(ach, 1),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4),
+                     "traffic": traffic, "algorithmic_bytes": abytes[dom],
+                     "avg_us": round(per[dom] * 1e3, 2)},
+        "layer_hbm_frac": round(layer_min_bytes(cfg) / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "stages": stages,
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle on a bounded sample ...", file=sys.stderr,
+              flush=True)
+        cb = cpu_baseline(cfg, inp, sc, args.cpu_budget_s)
+        result["cpu_baseline"] = cb
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

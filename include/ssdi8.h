@@ -1,0 +1,181 @@
+/*
+ * ssdi8.h — C ABI of the MI355X (gfx950) INT8 SSD chunk-scan library (libssdi8.so).
+ *
+ * The library computes the persistent-INT8 Mamba-2 SSD layer of "SSDi8: Accurate and Efficient
+ * 8-bit Quantization for State Space Duality": B and C quantized once per group (Sec. 4.2,
+ * "Quantization of B, C"), the chunk state as an INT8 x INT8 product after moving the decay
+ * table onto x (Eq. 7) with an INT32->INT8 requantisation (Eq. 8), INT8 state passing with a
+ * fixed-point decay and a k-bit shift (Eq. 9), INT8 ChunkBMM, INT8 ChunkScan1 with the decay
+ * applied after the product, FP16 ChunkScan2 with the CB dequant scale folded into its table,
+ * and an output epilogue adding the Mamba-2 D skip term and the per-channel correction term c of
+ * Eq. 10.
+ *
+ * Conventions shared by every entry point
+ *   - Tensor pointers are DEVICE pointers owned by the caller; the library never allocates or
+ *     frees device memory.  Scratch space is the caller's `workspace` (see
+ *     ssdi8_ssd_workspace_size).
+ *   - Every call is asynchronous on `stream` (a hipStream_t; NULL = the default stream) and
+ *     enqueues its kernels in order on that stream.  There is no hidden device synchronisation
+ *     and no global mutable state: calls on different streams are independent.
+ *   - All arguments are validated on the host BEFORE anything is enqueued; on any error nothing
+ *     is launched and no output is touched.  Launch failures return SSDI8_ERR_HIP.  Device-side
+ *     faults surface at the caller's next synchronisation.  Nothing is thrown across the ABI.
+ *   - Layouts are dense row-major (C order) in the paper's storage order (Sec. 4.1):
+ *     x, y [b, l, h, p];  dt [b, l, h];  A, D [h];  B, C [b, l, g, n].  Head h reads group
+ *     h / (H/G) (contiguous heads per group).
+ *   - Quantized integers are symmetric int8 in [-127, 127] (-128 is never produced).  A step
+ *     size ("scale") alpha maps an integer q to alpha * q (Eq. 1: alpha = absmax / 127).
+ *   - Supported shapes: headdim P = 64, dstate N = 128, chunk Q = 256; seqlen a multiple of the
+ *     chunk; nheads a multiple of ngroups.  Others return SSDI8_ERR_UNSUPPORTED / _SHAPE.
+ *   - Floating-point inputs containing NaN or Inf give unspecified (but in-bounds) results.
+ */
+#ifndef SSDI8_H
+#define SSDI8_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SSDI8_OK = 0,
+  SSDI8_ERR_NULL = 1,         /* a required pointer is NULL                                  */
+  SSDI8_ERR_SHAPE = 2,        /* inconsistent or negative sizes, L % chunk != 0, H % G != 0  */
+  SSDI8_ERR_UNSUPPORTED = 3,  /* valid but not implemented (P != 64, N != 128, chunk != 256) */
+  SSDI8_ERR_ALIGN = 4,        /* a tensor pointer is not 16-byte aligned                     */
+  SSDI8_ERR_WORKSPACE = 5,    /* workspace NULL or smaller than ssdi8_ssd_workspace_size     */
+  SSDI8_ERR_HIP = 6,          /* a kernel launch failed                                      */
+  SSDI8_ERR_ARG = 7           /* an enum / flag / shift argument is out of range             */
+} ssdi8_status;
+
+typedef enum { SSDI8_F32 = 0, SSDI8_F16 = 1 } ssdi8_dtype;
+
+/* Quantization granules of a logical [b, l, k, m] tensor. */
+typedef enum {
+  SSDI8_GRAN_TENSOR = 0,   /* one step for the whole tensor              scale[1]        */
+  SSDI8_GRAN_GROUP = 1,    /* one step per k (B, C: per group)           scale[k]        */
+  SSDI8_GRAN_CHANNEL = 2,  /* one step per (k, m) (x: per head, channel) scale[k*m]      */
+  SSDI8_GRAN_TOKEN = 3     /* one step per (b, l, k)                     scale[b*l*k]    */
+} ssdi8_gran;
+
+typedef struct {
+  int64_t batch, seqlen, nheads, headdim, ngroups, dstate, chunk;
+} ssdi8_dims;
+
+/*
+ * ssdi8_quantize_act — uniform symmetric 8-bit quantization of an activation (Eq. 1).
+ * Used for B and C once per layer, per group (Sec. 4.2 "Quantization of B, C"), before their
+ * reuse by ChunkState, ChunkBMM and ChunkScan1.
+ *
+ *   src      device, [b, l, k, m] of src_dtype (SSDI8_F16 or SSDI8_F32), 16-byte aligned.
+ *   gran     granule of one step size (ssdi8_gran).
+ *   scale    device fp32 step sizes, one per granule (sizes above).
+ *            compute_scale = 0: read (static calibration, the paper's setting);
+ *            compute_scale = 1: written with fl32(absmax / 127) of each granule (1 for an
+ *            all-zero granule), then used.  Dynamic TENSOR/GROUP/CHANNEL modes support at most
+ *            8192 granules (SSDI8_ERR_UNSUPPORTED beyond); TOKEN mode any number.
+ *   dst      device int8 [b, l, k, m], 16-byte aligned:
+ *            dst = clamp(rne(fl32(src * fl32(1 / scale))), -127, 127).
+ *   b*l == 0 is valid: src and dst may then be NULL; nothing is quantized (dynamic
+ *   TENSOR/GROUP/CHANNEL steps are set to 1, TOKEN has no steps).
+ * Errors: NULL scale, NULL src/dst with b*l > 0, negative b/l, k or m < 1, bad dtype/gran,
+ * misalignment (src, dst 16 bytes; scale 4 bytes).
+ */
+ssdi8_status ssdi8_quantize_act(const void* src, int src_dtype, int64_t b, int64_t l, int64_t k,
+                                int64_t m, int gran, float* scale, int compute_scale, int8_t* dst,
+                                void* stream);
+
+/*
+ * ssdi8_state_pass — INT8 StatePassing across chunks (Eq. 9, Alg. 2 module 3):
+ *     P_in[0] = init (zeros if init_q is NULL)
+ *     P_in[c+1] = clamp(S_q[c] + ((q_d[c] * P_in[c] + r) >> shift), -127, 127)
+ * with r = 2^(shift-1) when shift_round != 0 and r = 0 otherwise, int32 arithmetic with an
+ * arithmetic right shift.  One step size per (h, p) is shared by all chunks, which is what makes
+ * the integer recurrence valid (Sec. 4.2).
+ *
+ *   state_q     device int8 [batch, nchunks, nheads, headdim, dstate]: chunk-local states.
+ *   decay_q     device int16 [batch, nheads, nchunks]: Q(Decay) = rne(exp(dA_cs_last) 2^shift),
+ *               normally in [0, 2^shift]; other values are used as given.
+ *   shift       k in [1, 14] (the paper uses 7).
+ *   init_q      device int8 [batch, nheads, headdim, dstate] or NULL.
+ *   state_in_q  device int8 [batch, nchunks, nheads, headdim, dstate]: P_in[c], the state
+ *               ENTERING chunk c (read by ChunkScan1 of chunk c).
+ *   final_q     device int8 [batch, nheads, headdim, dstate] = P_in[nchunks], or NULL.
+ *   final_state device fp32 same shape = fl32(final_q * state_scale[h, p]), or NULL
+ *               (state_scale must then be non-NULL, [nheads, headdim]).
+ * nchunks == 0 copies init (or zeros) to the final outputs.  Pointers 16-byte aligned.
+ */
+ssdi8_status ssdi8_state_pass(const int8_t* state_q, const int16_t* decay_q, int shift,
+                              int shift_round, const int8_t* init_q, int8_t* state_in_q,
+                              int8_t* final_q, float* final_state, const float* state_scale,
+                              int64_t batch, int64_t nchunks, int64_t nheads, int64_t headdim,
+                              int64_t dstate, void* stream);
+
+/*
+ * Arguments of ssdi8_ssd_chunk_scan (Alg. 2 with the SSDi8 quantization of Sec. 4.2).
+ * Sizes come from ssdi8_dims: B = batch, L = seqlen, H = nheads, P = headdim, G = ngroups,
+ * N = dstate, Q = chunk, c = L / Q.  All pointers are device pointers, 16-byte aligned.
+ */
+typedef struct {
+  const void* x;  int x_dtype;        /* [B,L,H,P] fp16 or fp32                                  */
+  const float* dt; int dt_softplus;   /* [B,L,H]; if dt_softplus, softplus is applied first      */
+                                      /*   (fp64, threshold 20, rounded once to fp32)            */
+  const float* A;                     /* [H] decay parameter (<= 0)                              */
+  const int8_t* Bq;                   /* [B,L,G,N] from ssdi8_quantize_act, per-group steps      */
+  const int8_t* Cq;                   /* [B,L,G,N] per-group steps, or per-token steps           */
+  const float* B_scale;               /* [G]                                                     */
+  const float* C_scale;               /* [G], or [B,L,G] when c_per_token != 0                   */
+  int c_per_token;
+  const float* D;                     /* [H] skip term, or NULL (= 0)                            */
+  const float* corr;                  /* [H,P] per-channel correction c (Eq. 10), or NULL (= 0)  */
+  const float* xs_scale;              /* step of X_scaled = LUT_state * x (Eq. 7): [H,P], or [H] */
+  int xs_per_head;                    /*   when xs_per_head != 0                                 */
+  const float* state_scale;           /* [H,P] step of the int8 states (Eq. 8, shared over c)    */
+  const float* cb_scale;              /* [G] step of the int8 C.B^T                              */
+  int decay_shift;                    /* k of Eq. 9, in [1, 14]; the paper uses 7                */
+  int shift_round;                    /* 1: add 2^(k-1) before the shift; 0: floor shift         */
+  const int8_t* init_state_q;         /* [B,H,P,N] int8 initial state at state_scale, or NULL    */
+  void* y; int y_dtype;               /* [B,L,H,P] output, fp16 or fp32                          */
+  int8_t* final_state_q;              /* [B,H,P,N] or NULL                                       */
+  float* final_state;                 /* [B,H,P,N] fp32 = final_state_q * state_scale, or NULL   */
+  /* Optional intermediate outputs (NULL = not produced), in the layouts listed: */
+  int8_t* xs_q;                       /* [B,L,H,P]   Q(X_scaled)                                 */
+  int32_t* state_i32;                 /* [B,c,H,P,N] State_INT32 (Eq. 7)                         */
+  int8_t* state_q;                    /* [B,c,H,P,N] State_INT8 (Eq. 8), chunk-local             */
+  int16_t* decay_q;                   /* [B,H,c]     Q(Decay) (Eq. 9)                            */
+  int8_t* state_in_q;                 /* [B,c,H,P,N] state entering each chunk after passing     */
+  int32_t* cb_i32;                    /* [B,c,G,Q,Q] C.B^T int32, entries i <= j only            */
+  int8_t* cb_q;                       /* [B,c,G,Q,Q] C.B^T int8, entries i <= j only             */
+  int32_t* scan1_i32;                 /* [B,L,H,P]   C_q . P_in^T int32 (ChunkScan1 product)     */
+  void* workspace; size_t workspace_bytes;
+  /* Optional per-module timing: NULL, or 5 hipEvent_t handles created by the caller; they are
+     recorded on `stream` before ChunkBMM, before ChunkState, before StatePassing, before
+     ChunkScan and after ChunkScan (the module breakdown of the paper's latency figures). */
+  void* const* stage_events;
+} ssdi8_scan_args;
+
+/* Workspace bytes needed by ssdi8_ssd_chunk_scan for these sizes (0 on invalid sizes). */
+size_t ssdi8_ssd_workspace_size(const ssdi8_dims* d);
+
+/*
+ * ssdi8_ssd_chunk_scan — one SSD layer: ChunkCumsum, ChunkState, StatePassing, ChunkBMM,
+ * ChunkScan1 + ChunkScan2 and the output epilogue
+ *     y = y_off + y_diag + D[h] x + corr[h, p]
+ * (Alg. 2 modules 1-6, Eq. 7-9, Eq. 10 correction applied at the SSD output).  B and C must
+ * already be quantized (ssdi8_quantize_act).  Intermediates go through `workspace`.
+ */
+ssdi8_status ssdi8_ssd_chunk_scan(const ssdi8_dims* d, const ssdi8_scan_args* a, void* stream);
+
+/* Static description of a status code. */
+const char* ssdi8_status_string(int status);
+
+/* Library version, e.g. "0.1.0". */
+const char* ssdi8_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SSDI8_H */

@@ -1,0 +1,207 @@
+// C ABI of libssdi8 (declared in include/ssdi8.h): argument validation, workspace planning and
+// in-order kernel launches on the caller's stream.
+#include "ssdi8.h"
+
+#include <hip/hip_runtime.h>
+
+#include "common.hpp"
+#include "launch.hpp"
+
+namespace {
+
+using ssdi8::LayerDims;
+
+constexpr int64_t kMaxDim = (int64_t)1 << 31;
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+bool aligned16_or_null(const void* p) { return p == nullptr || aligned16(p); }
+
+size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+struct Plan {
+  size_t bqT, sq, pin, cbq, qd, total;
+};
+
+// Workspace regions (256-byte aligned): B_q^T chunks, chunk-local int8 states, entering int8
+// states, int8 C.B^T, int16 Q(Decay).
+Plan plan_workspace(const ssdi8_dims* d) {
+  const size_t B = (size_t)d->batch, L = (size_t)d->seqlen, H = (size_t)d->nheads;
+  const size_t P = (size_t)d->headdim, G = (size_t)d->ngroups, N = (size_t)d->dstate;
+  const size_t Q = (size_t)d->chunk, nc = L / Q;
+  Plan p;
+  size_t off = 0;
+  p.bqT = off; off = round_up(off + B * L * G * N, 256);
+  p.sq = off;  off = round_up(off + B * nc * H * P * N, 256);
+  p.pin = off; off = round_up(off + B * nc * H * P * N, 256);
+  p.cbq = off; off = round_up(off + B * nc * G * Q * Q, 256);
+  p.qd = off;  off = round_up(off + B * H * nc * sizeof(int16_t), 256);
+  p.total = off;
+  return p;
+}
+
+ssdi8_status check_dims(const ssdi8_dims* d) {
+  if (!d) return SSDI8_ERR_NULL;
+  if (d->batch < 0 || d->seqlen < 0 || d->nheads < 1 || d->headdim < 1 || d->ngroups < 1 ||
+      d->dstate < 1 || d->chunk < 1)
+    return SSDI8_ERR_SHAPE;
+  if (d->batch >= kMaxDim || d->seqlen >= kMaxDim || d->nheads >= kMaxDim ||
+      d->ngroups >= kMaxDim)
+    return SSDI8_ERR_SHAPE;
+  if (d->nheads % d->ngroups != 0 || d->seqlen % d->chunk != 0) return SSDI8_ERR_SHAPE;
+  if (d->headdim != ssdi8::kP || d->dstate != ssdi8::kN || d->chunk != ssdi8::kQ)
+    return SSDI8_ERR_UNSUPPORTED;
+  // element counts of the largest tensors must stay addressable and grids launchable
+  const double xel = (double)d->batch * d->seqlen * d->nheads * d->headdim;
+  if (xel > 4.0e12) return SSDI8_ERR_SHAPE;
+  const double nwork = (double)d->batch * (d->seqlen / d->chunk) * d->nheads;
+  if (nwork >= 2147483647.0) return SSDI8_ERR_SHAPE;
+  return SSDI8_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* ssdi8_version(void) { return "0.1.0"; }
+
+const char* ssdi8_status_string(int s) {
+  switch (s) {
+    case SSDI8_OK: return "ok";
+    case SSDI8_ERR_NULL: return "required pointer is NULL";
+    case SSDI8_ERR_SHAPE: return "invalid or inconsistent sizes";
+    case SSDI8_ERR_UNSUPPORTED: return "sizes not supported (need headdim 64, dstate 128, chunk 256)";
+    case SSDI8_ERR_ALIGN: return "tensor pointer not 16-byte aligned";
+    case SSDI8_ERR_WORKSPACE: return "workspace missing or too small";
+    case SSDI8_ERR_HIP: return "HIP kernel launch failed";
+    case SSDI8_ERR_ARG: return "argument out of range";
+    default: return "unknown status";
+  }
+}
+
+ssdi8_status ssdi8_quantize_act(const void* src, int src_dtype, int64_t b, int64_t l, int64_t k,
+                                int64_t m, int gran, float* scale, int compute_scale, int8_t* dst,
+                                void* stream) {
+  if (src_dtype != SSDI8_F32 && src_dtype != SSDI8_F16) return SSDI8_ERR_ARG;
+  if (gran < SSDI8_GRAN_TENSOR || gran > SSDI8_GRAN_TOKEN) return SSDI8_ERR_ARG;
+  if (b < 0 || l < 0 || k < 1 || m < 1) return SSDI8_ERR_SHAPE;
+  if (b >= kMaxDim || l >= kMaxDim || k >= kMaxDim || m >= kMaxDim) return SSDI8_ERR_SHAPE;
+  if ((double)b * l * k * m > 4.0e12) return SSDI8_ERR_SHAPE;
+  const bool empty = (b == 0 || l == 0);
+  if (!scale || (!empty && (!src || !dst))) return SSDI8_ERR_NULL;
+  if (!aligned16_or_null(src) || !aligned16_or_null(dst) || ((uintptr_t)scale & 3u))
+    return SSDI8_ERR_ALIGN;
+  if (compute_scale && gran != SSDI8_GRAN_TOKEN) {
+    const int64_t ngran = gran == SSDI8_GRAN_TENSOR ? 1 : (gran == SSDI8_GRAN_GROUP ? k : k * m);
+    if (ngran > ssdi8::quantize_max_granules()) return SSDI8_ERR_UNSUPPORTED;
+  }
+  hipError_t e = ssdi8::launch_quantize(src, src_dtype, b, l, k, m, gran, scale, compute_scale,
+                                        dst, (hipStream_t)stream);
+  return e == hipSuccess ? SSDI8_OK : SSDI8_ERR_HIP;
+}
+
+ssdi8_status ssdi8_state_pass(const int8_t* state_q, const int16_t* decay_q, int shift,
+                              int shift_round, const int8_t* init_q, int8_t* state_in_q,
+                              int8_t* final_q, float* final_state, const float* state_scale,
+                              int64_t batch, int64_t nchunks, int64_t nheads, int64_t headdim,
+                              int64_t dstate, void* stream) {
+  if (batch < 0 || nchunks < 0 || nheads < 1 || headdim < 1 || dstate < 1)
+    return SSDI8_ERR_SHAPE;
+  if (batch >= kMaxDim || nchunks >= kMaxDim || nheads >= kMaxDim || headdim >= kMaxDim ||
+      dstate >= kMaxDim)
+    return SSDI8_ERR_SHAPE;
+  if ((double)batch * nchunks * nheads * headdim * dstate > 4.0e12) return SSDI8_ERR_SHAPE;
+  if (shift < 1 || shift > 14) return SSDI8_ERR_ARG;
+  if (nchunks > 0 && (!state_q || !decay_q || !state_in_q)) return SSDI8_ERR_NULL;
+  if (final_state && !state_scale) return SSDI8_ERR_NULL;
+  if (dstate % 4 != 0) return SSDI8_ERR_UNSUPPORTED;
+  if (!aligned16_or_null(state_q) || !aligned16_or_null(state_in_q) ||
+      !aligned16_or_null(init_q) || !aligned16_or_null(final_q) ||
+      !aligned16_or_null(final_state) || ((uintptr_t)decay_q & 1u))
+    return SSDI8_ERR_ALIGN;
+  hipError_t e = ssdi8::launch_state_pass(batch, nchunks, nheads, headdim * dstate, headdim,
+                                          state_q, decay_q, shift, shift_round, init_q,
+                                          state_in_q, final_q, final_state, state_scale,
+                                          (hipStream_t)stream);
+  return e == hipSuccess ? SSDI8_OK : SSDI8_ERR_HIP;
+}
+
+size_t ssdi8_ssd_workspace_size(const ssdi8_dims* d) {
+  if (check_dims(d) != SSDI8_OK) return 0;
+  return plan_workspace(d).total;
+}
+
+ssdi8_status ssdi8_ssd_chunk_scan(const ssdi8_dims* d, const ssdi8_scan_args* a, void* stream) {
+  ssdi8_status s = check_dims(d);
+  if (s != SSDI8_OK) return s;
+  if (!a) return SSDI8_ERR_NULL;
+  if (a->x_dtype != SSDI8_F32 && a->x_dtype != SSDI8_F16) return SSDI8_ERR_ARG;
+  if (a->y_dtype != SSDI8_F32 && a->y_dtype != SSDI8_F16) return SSDI8_ERR_ARG;
+  if (a->decay_shift < 1 || a->decay_shift > 14) return SSDI8_ERR_ARG;
+  const bool work = d->batch > 0 && d->seqlen > 0;
+  if (work && (!a->x || !a->dt || !a->A || !a->Bq || !a->Cq || !a->B_scale || !a->C_scale ||
+               !a->xs_scale || !a->state_scale || !a->cb_scale || !a->y))
+    return SSDI8_ERR_NULL;
+  if (a->final_state && !a->state_scale) return SSDI8_ERR_NULL;
+  const void* al[] = {a->x, a->y, a->Bq, a->Cq, a->init_state_q, a->final_state_q,
+                      a->final_state, a->xs_q, a->state_i32, a->state_q, a->decay_q,
+                      a->state_in_q, a->cb_i32, a->cb_q, a->scan1_i32, a->workspace};
+  for (const void* p : al)
+    if (!aligned16_or_null(p)) return SSDI8_ERR_ALIGN;
+  const Plan plan = plan_workspace(d);
+  if (work && (!a->workspace || a->workspace_bytes < plan.total)) return SSDI8_ERR_WORKSPACE;
+  if (a->stage_events)
+    for (int i = 0; i < 5; ++i)
+      if (!a->stage_events[i]) return SSDI8_ERR_NULL;
+
+  hipStream_t st = (hipStream_t)stream;
+  LayerDims ld;
+  ld.batch = (int)d->batch;
+  ld.seqlen = (int)d->seqlen;
+  ld.nheads = (int)d->nheads;
+  ld.ngroups = (int)d->ngroups;
+  ld.nchunks = (int)(d->seqlen / d->chunk);
+  const int64_t elems = d->headdim * d->dstate;
+
+  if (!work) {
+    // no tokens: the final state is the initial state
+    if (d->batch > 0 && (a->final_state_q || a->final_state)) {
+      hipError_t e = ssdi8::launch_state_pass(d->batch, 0, d->nheads, elems, d->headdim,
+                                              nullptr, nullptr, a->decay_shift, a->shift_round,
+                                              a->init_state_q, nullptr, a->final_state_q,
+                                              a->final_state, a->state_scale, st);
+      if (e != hipSuccess) return SSDI8_ERR_HIP;
+    }
+    return SSDI8_OK;
+  }
+
+  char* ws = static_cast<char*>(a->workspace);
+  int8_t* bqT = reinterpret_cast<int8_t*>(ws + plan.bqT);
+  int8_t* sq = a->state_q ? a->state_q : reinterpret_cast<int8_t*>(ws + plan.sq);
+  int8_t* pin = a->state_in_q ? a->state_in_q : reinterpret_cast<int8_t*>(ws + plan.pin);
+  int8_t* cbq = a->cb_q ? a->cb_q : reinterpret_cast<int8_t*>(ws + plan.cbq);
+  int16_t* qd = a->decay_q ? a->decay_q : reinterpret_cast<int16_t*>(ws + plan.qd);
+
+  auto mark = [&](int i) -> bool {
+    return !a->stage_events ||
+           hipEventRecord(static_cast<hipEvent_t>(a->stage_events[i]), st) == hipSuccess;
+  };
+  if (!mark(0)) return SSDI8_ERR_HIP;
+  hipError_t e = ssdi8::launch_chunk_bmm(ld, a->Cq, a->Bq, a->C_scale, a->c_per_token,
+                                         a->B_scale, a->cb_scale, cbq, a->cb_i32, bqT, st);
+  if (e != hipSuccess || !mark(1)) return SSDI8_ERR_HIP;
+  e = ssdi8::launch_chunk_state(ld, a->x, a->x_dtype, a->dt, a->dt_softplus, a->A, bqT,
+                                a->B_scale, a->xs_scale, a->xs_per_head, a->state_scale,
+                                a->decay_shift, sq, qd, a->xs_q, a->state_i32, st);
+  if (e != hipSuccess || !mark(2)) return SSDI8_ERR_HIP;
+  e = ssdi8::launch_state_pass(d->batch, ld.nchunks, d->nheads, elems, d->headdim, sq, qd,
+                               a->decay_shift, a->shift_round, a->init_state_q, pin,
+                               a->final_state_q, a->final_state, a->state_scale, st);
+  if (e != hipSuccess || !mark(3)) return SSDI8_ERR_HIP;
+  e = ssdi8::launch_chunk_scan(ld, a->x, a->x_dtype, a->dt, a->dt_softplus, a->A, a->Cq,
+                               a->C_scale, a->c_per_token, pin, cbq, a->cb_scale, a->state_scale,
+                               a->D, a->corr, a->y, a->y_dtype, a->scan1_i32, st);
+  if (e != hipSuccess || !mark(4)) return SSDI8_ERR_HIP;
+  return SSDI8_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,79 @@
+// Device helpers shared by the gfx950 kernels of libssdi8.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ssdi8 {
+
+// Fixed problem geometry of the kernels: headdim P, state size N, chunk length Q.
+constexpr int kP = 64;
+constexpr int kN = 128;
+constexpr int kQ = 256;
+constexpr int kQMax = 127;
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+typedef int v16i __attribute__((ext_vector_type(16)));
+typedef float v16f __attribute__((ext_vector_type(16)));
+typedef _Float16 v8h __attribute__((ext_vector_type(8)));
+
+// Symmetric int8 quantization of an fp32 value with a precomputed inverse step:
+// clamp(rne(v * inv), -127, 127).  One IEEE fp32 product, round-half-even to integer.
+__device__ __forceinline__ int quant_i8(float v, float inv) {
+  float p = v * inv;
+  float r = __builtin_rintf(p);
+  r = __builtin_fminf(__builtin_fmaxf(r, -127.0f), 127.0f);
+  return (int)r;
+}
+
+// INT32 accumulator -> int8 with an fp32 multiplier: clamp(rne(fl32(acc) * m)).
+__device__ __forceinline__ int requant_i8(int acc, float m) {
+  return quant_i8((float)acc, m);
+}
+
+// softplus in fp64 with the usual threshold, rounded once to fp32.
+__device__ __forceinline__ float softplus_f32(float v) {
+  double d = (double)v;
+  return (float)(d > 20.0 ? d : log1p(exp(d)));
+}
+
+// Map a linear block id to a work index so that consecutive work items land on the same XCD.
+// Workgroups are dispatched round-robin over the 8 XCDs of the chip; this inverts that so
+// each XCD owns one contiguous range of work (neighbouring heads of one chunk share B, C and
+// CB tiles through that XCD's L2).
+__device__ __forceinline__ int xcd_remap(int bid, int nwg) {
+  constexpr int kXcd = 8;
+  int q = nwg / kXcd, r = nwg % kXcd;
+  int xcd = bid % kXcd, idx = bid / kXcd;
+  return (xcd < r) ? xcd * (q + 1) + idx : r * (q + 1) + (xcd - r) * q + idx;
+}
+
+// Inclusive prefix sum over the 256 threads of a block in fp64.  The in-chunk sums of fp32
+// decay increments are exact in fp64 (the terms of one chunk span few binades), so the tree
+// order used here gives the same values as a sequential sum.  `scratch` holds 4 doubles.
+__device__ __forceinline__ double block_scan_f64_256(double v, double* scratch) {
+  const int lane = threadIdx.x & 63;
+  const int w = threadIdx.x >> 6;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    double t = __shfl_up(v, off, 64);
+    if (lane >= off) v += t;
+  }
+  if (lane == 63) scratch[w] = v;
+  __syncthreads();
+  double pre = 0.0;
+  for (int i = 0; i < w; ++i) pre += scratch[i];
+  return v + pre;
+}
+
+// Pack the low bytes of four ints into one dword (byte i = v_i).
+__device__ __forceinline__ uint32_t pack4_i8(int v0, int v1, int v2, int v3) {
+  return (uint32_t)(v0 & 0xff) | ((uint32_t)(v1 & 0xff) << 8) | ((uint32_t)(v2 & 0xff) << 16) |
+         ((uint32_t)(v3 & 0xff) << 24);
+}
+
+__device__ __forceinline__ int sext8(uint32_t w, int byte) {
+  return (int)(int8_t)((w >> (8 * byte)) & 0xffu);
+}
+
+}  // namespace ssdi8

@@ -1,0 +1,196 @@
+// Activation quantization (Eq. 1): static steps, or dynamic absmax/127 steps per granule.
+// Used for B and C once per layer along the group axis (Sec. 4.2) and, in TOKEN mode, for
+// per-token C steps (one wavefront reduction per token row).
+#include "common.hpp"
+#include "launch.hpp"
+
+namespace ssdi8 {
+
+namespace {
+
+template <typename T>
+__device__ __forceinline__ float ld_f32(const T* p, int64_t i) {
+  return (float)p[i];
+}
+
+__device__ __forceinline__ int64_t granule_of(int64_t e, int gran, int64_t k, int64_t m) {
+  int64_t row = e / m;
+  switch (gran) {
+    case 0: return 0;                // tensor
+    case 1: return row % k;          // group
+    case 2: return e % (k * m);      // channel
+    default: return row;             // token
+  }
+}
+
+// 16 consecutive elements per thread; requires m % 16 == 0 (all 16 share one (b,l,k) row).
+template <typename T>
+__global__ __launch_bounds__(256) void quant_static_vec16(const T* __restrict__ src,
+                                                          int8_t* __restrict__ dst,
+                                                          const float* __restrict__ scale,
+                                                          int gran, int64_t nvec, int64_t k,
+                                                          int64_t m) {
+  for (int64_t v = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; v < nvec;
+       v += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t e0 = v * 16;
+    float x[16];
+    if constexpr (sizeof(T) == 2) {
+      const uint4* s = reinterpret_cast<const uint4*>(src + e0);
+      uint4 a = s[0], b = s[1];
+      const _Float16* ha = reinterpret_cast<const _Float16*>(&a);
+      const _Float16* hb = reinterpret_cast<const _Float16*>(&b);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        x[i] = (float)ha[i];
+        x[8 + i] = (float)hb[i];
+      }
+    } else {
+      const float4* s = reinterpret_cast<const float4*>(src + e0);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        float4 f = s[i];
+        x[4 * i] = f.x; x[4 * i + 1] = f.y; x[4 * i + 2] = f.z; x[4 * i + 3] = f.w;
+      }
+    }
+    int q[16];
+    if (gran == 2) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) q[i] = quant_i8(x[i], 1.0f / scale[(e0 + i) % (k * m)]);
+    } else {
+      const float inv = 1.0f / scale[granule_of(e0, gran, k, m)];
+#pragma unroll
+      for (int i = 0; i < 16; ++i) q[i] = quant_i8(x[i], inv);
+    }
+    uint4 o;
+    o.x = pack4_i8(q[0], q[1], q[2], q[3]);
+    o.y = pack4_i8(q[4], q[5], q[6], q[7]);
+    o.z = pack4_i8(q[8], q[9], q[10], q[11]);
+    o.w = pack4_i8(q[12], q[13], q[14], q[15]);
+    *reinterpret_cast<uint4*>(dst + e0) = o;
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void quant_static_scalar(const T* __restrict__ src,
+                                                           int8_t* __restrict__ dst,
+                                                           const float* __restrict__ scale,
+                                                           int gran, int64_t n, int64_t k,
+                                                           int64_t m) {
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n;
+       e += (int64_t)gridDim.x * blockDim.x) {
+    dst[e] = (int8_t)quant_i8(ld_f32(src, e), 1.0f / scale[granule_of(e, gran, k, m)]);
+  }
+}
+
+__global__ void fill_u32(uint32_t* p, int64_t n, uint32_t v) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = v;
+}
+
+// Absolute maximum per granule (tensor / group / channel, at most kMaxGranules granules),
+// accumulated as the bit patterns of non-negative floats (their integer order is the float
+// order) with LDS and then global atomic max into `acc` (pre-zeroed).
+constexpr int kMaxGranules = 8192;
+
+template <typename T>
+__global__ __launch_bounds__(256) void absmax_granules(const T* __restrict__ src,
+                                                       uint32_t* __restrict__ acc, int gran,
+                                                       int64_t n, int64_t k, int64_t m,
+                                                       int ngran) {
+  __shared__ uint32_t smax[kMaxGranules];
+  for (int i = threadIdx.x; i < ngran; i += blockDim.x) smax[i] = 0u;
+  __syncthreads();
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n;
+       e += (int64_t)gridDim.x * blockDim.x) {
+    float a = __builtin_fabsf(ld_f32(src, e));
+    atomicMax(&smax[granule_of(e, gran, k, m)], __float_as_uint(a));
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < ngran; i += blockDim.x)
+    if (smax[i]) atomicMax(&acc[i], smax[i]);
+}
+
+__global__ void absmax_to_step(float* scale, int n) {
+  int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) {
+    float a = __uint_as_float(__float_as_uint(scale[i])) / 127.0f;
+    scale[i] = (a == 0.0f) ? 1.0f : a;
+  }
+}
+
+// TOKEN granularity, dynamic: one wavefront per (b,l,k) row of m elements.
+template <typename T>
+__global__ __launch_bounds__(256) void quant_token_dynamic(const T* __restrict__ src,
+                                                           int8_t* __restrict__ dst,
+                                                           float* __restrict__ scale,
+                                                           int64_t rows, int64_t m) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const T* s = src + row * m;
+  float mx = 0.0f;
+  for (int64_t i = lane; i < m; i += 64) mx = __builtin_fmaxf(mx, __builtin_fabsf((float)s[i]));
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) mx = __builtin_fmaxf(mx, __shfl_xor(mx, off, 64));
+  float a = mx / 127.0f;
+  a = (a == 0.0f) ? 1.0f : a;
+  if (lane == 0) scale[row] = a;
+  const float inv = 1.0f / a;
+  for (int64_t i = lane; i < m; i += 64) dst[row * m + i] = (int8_t)quant_i8((float)s[i], inv);
+}
+
+inline int64_t grid_for(int64_t items, int per_block = 256, int64_t cap = 65536) {
+  int64_t g = (items + per_block - 1) / per_block;
+  return g < 1 ? 1 : (g > cap ? cap : g);
+}
+
+template <typename T>
+hipError_t quantize_impl(const T* src, int64_t b, int64_t l, int64_t k, int64_t m, int gran,
+                         float* scale, int compute_scale, int8_t* dst, hipStream_t st) {
+  const int64_t n = b * l * k * m;
+  if (compute_scale && gran == 3) {
+    const int64_t rows = b * l * k;
+    if (rows == 0) return hipSuccess;
+    hipLaunchKernelGGL(quant_token_dynamic<T>, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0,
+                       st, src, dst, scale, rows, m);
+    return hipGetLastError();
+  }
+  if (compute_scale) {
+    const int ngran = gran == 0 ? 1 : (gran == 1 ? (int)k : (int)(k * m));
+    hipLaunchKernelGGL(fill_u32, dim3((unsigned)grid_for(ngran)), dim3(256), 0, st,
+                       reinterpret_cast<uint32_t*>(scale), (int64_t)ngran, 0u);
+    if (n > 0) {
+      hipLaunchKernelGGL(absmax_granules<T>, dim3((unsigned)grid_for(n, 256, 2048)), dim3(256),
+                         0, st, src, reinterpret_cast<uint32_t*>(scale), gran, n, k, m, ngran);
+    }
+    hipLaunchKernelGGL(absmax_to_step, dim3((unsigned)((ngran + 255) / 256)), dim3(256), 0, st,
+                       scale, ngran);
+  }
+  if (n == 0) return hipGetLastError();
+  if (m % 16 == 0) {
+    const int64_t nvec = n / 16;
+    hipLaunchKernelGGL(quant_static_vec16<T>, dim3((unsigned)grid_for(nvec)), dim3(256), 0, st,
+                       src, dst, scale, gran, nvec, k, m);
+  } else {
+    hipLaunchKernelGGL(quant_static_scalar<T>, dim3((unsigned)grid_for(n)), dim3(256), 0, st,
+                       src, dst, scale, gran, n, k, m);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace
+
+int quantize_max_granules() { return kMaxGranules; }
+
+hipError_t launch_quantize(const void* src, int src_dtype, int64_t b, int64_t l, int64_t k,
+                           int64_t m, int gran, float* scale, int compute_scale, int8_t* dst,
+                           hipStream_t st) {
+  if (src_dtype == 1)
+    return quantize_impl(static_cast<const _Float16*>(src), b, l, k, m, gran, scale,
+                         compute_scale, dst, st);
+  return quantize_impl(static_cast<const float*>(src), b, l, k, m, gran, scale, compute_scale,
+                       dst, st);
+}
+
+}  // namespace ssdi8

@@ -1,0 +1,288 @@
+"""GPU parity of the HIP path (through the C ABI) against the CPU oracle.
+
+Integer stages are compared bit for bit, each on the GPU's own inputs to that stage (stage
+isolation), and end to end against the oracle's own chain; the floating-point output is held to
+max|dy|/max|y| <= 1e-2 and relative L2 <= 1e-3."""
+import numpy as np
+import pytest
+
+from helpers import assert_close, calibration, check_slab, dev, run_layer, say
+from oracle import exact as oex
+from oracle import int8 as oq
+from paper_2608_21952_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+ALL_TAPS = ("xs_q", "state_i32", "state_q", "decay_q", "state_in_q", "cb_i32", "cb_q",
+            "scan1_i32")
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as _t
+    assert _t.cuda.is_available(), "GPU tests need a GPU"
+    return _t
+
+
+@pytest.fixture(scope="module")
+def ssdi8(torch):
+    from paper_2608_21952_amd import ssdi8 as _s
+    _s.lib()
+    return _s
+
+
+# ---------------------------------------------------------------------------- quantize_act
+@pytest.mark.parametrize("dtype", [np.float16, np.float32])
+@pytest.mark.parametrize("gran", ["tensor", "group", "channel", "token"])
+def test_quantize_dynamic_and_static(torch, ssdi8, dtype, gran):
+    say(f"quantize_act dtype={dtype.__name__} gran={gran}")
+    rng = np.random.default_rng(1)
+    src = (rng.standard_normal((3, 40, 4, 128)) * np.exp(rng.uniform(-3, 3, (1, 1, 4, 1))))
+    src[:, :, :, 5] *= 20
+    src[1, 3] = 0
+    src = src.astype(dtype)
+    q_ref, a_ref = oq.quantize_act(src, gran)
+    q, a = ssdi8.quantize_act(dev(src, torch), gran)
+    torch.cuda.synchronize()
+    assert np.array_equal(a.cpu().numpy().reshape(np.shape(a_ref)), a_ref)
+    assert np.array_equal(q.cpu().numpy(), q_ref)
+    q2, _ = ssdi8.quantize_act(dev(src, torch), gran, a)
+    assert np.array_equal(q2.cpu().numpy(), q_ref)
+
+
+@pytest.mark.parametrize("m", [128, 24, 7])
+def test_quantize_odd_row_lengths(torch, ssdi8, m):
+    say(f"quantize_act m={m}")
+    rng = np.random.default_rng(2)
+    src = rng.standard_normal((2, 33, 3, m)).astype(np.float16)
+    alpha = np.array([0.01, 0.02, 0.5], np.float32)
+    q, _ = ssdi8.quantize_act(dev(src, torch), "group", dev(alpha, torch))
+    assert np.array_equal(q.cpu().numpy(), oq.quantize_act(src, "group", alpha)[0])
+
+
+def test_quantize_saturates_and_empty(torch, ssdi8):
+    src = np.array([[[[1000.0, -1000.0, 0.5, -0.5, 1.5, 2.5] + [0.0] * 10]]], np.float32)
+    q, _ = ssdi8.quantize_act(dev(src, torch), "tensor", dev(np.ones(1, np.float32), torch))
+    assert q.cpu().numpy().ravel()[:6].tolist() == [127, -127, 0, 0, 2, 2]
+    e, a = ssdi8.quantize_act(torch.zeros((0, 5, 2, 16), dtype=torch.float16, device="cuda"),
+                              "group")
+    torch.cuda.synchronize()
+    assert e.shape == (0, 5, 2, 16) and a.cpu().numpy().tolist() == [1.0, 1.0]
+
+
+# ---------------------------------------------------------------------------- state_pass
+@pytest.mark.parametrize("shift_round", [True, False])
+@pytest.mark.parametrize("shape", [(2, 9, 3, 64, 128), (1, 1, 1, 64, 128), (3, 40, 2, 8, 4),
+                                   (1, 70, 1, 64, 128)])
+def test_state_pass_bitexact(torch, ssdi8, shape, shift_round):
+    say(f"state_pass shape={shape} round={shift_round}")
+    rng = np.random.default_rng(3)
+    b, c, h, p, n = shape
+    sq = rng.integers(-127, 128, shape).astype(np.int8)
+    qd = rng.integers(0, 129, (b, h, c)).astype(np.int16)
+    qd[:, :, ::5] = 128
+    qd[:, :, 1::7] = 0
+    init = rng.integers(-127, 128, (b, h, p, n)).astype(np.int8)
+    scale = rng.uniform(0.01, 1.0, (h, p)).astype(np.float32)
+    out = ssdi8.state_pass(dev(sq, torch), dev(qd, torch), 7, shift_round, dev(init, torch),
+                           dev(scale, torch))
+    torch.cuda.synchronize()
+    pin_ref = np.empty_like(sq)
+    fin_ref = np.empty((b, h, p, n), np.int8)
+    for bi in range(b):
+        for hi in range(h):
+            pr, fr = oq.state_pass(sq[bi, :, hi], qd[bi, hi], init[bi, hi], 7, shift_round)
+            pin_ref[bi, :, hi] = pr
+            fin_ref[bi, hi] = fr
+    assert np.array_equal(out["state_in_q"].cpu().numpy(), pin_ref)
+    assert np.array_equal(out["final_q"].cpu().numpy(), fin_ref)
+    assert np.array_equal(out["final_state"].cpu().numpy(),
+                          fin_ref.astype(np.float32) * scale[None, :, :, None])
+
+
+def test_state_pass_zero_chunks_copies_init(torch, ssdi8):
+    rng = np.random.default_rng(4)
+    init = rng.integers(-127, 128, (2, 3, 64, 128)).astype(np.int8)
+    out = ssdi8.state_pass(torch.zeros((2, 0, 3, 64, 128), dtype=torch.int8, device="cuda"),
+                           torch.zeros((2, 3, 0), dtype=torch.int16, device="cuda"), 7, True,
+                           dev(init, torch))
+    assert np.array_equal(out["final_q"].cpu().numpy(), init)
+
+
+# ---------------------------------------------------------------------------- whole layer
+def _check_all(g, inp, sc, cfg, **kw):
+    for b in range(inp["x"].shape[0]):
+        for h in range(inp["x"].shape[2]):
+            check_slab(g, inp, sc, b, h, cfg.chunk, **kw)
+
+
+def test_layer_tiny_all_stages(torch, ssdi8):
+    cfg = synth.CONFIGS["tiny"]
+    say(f"layer {cfg.name}: B={cfg.batch} L={cfg.seqlen} H={cfg.nheads} G={cfg.ngroups} fp32")
+    inp = synth.draw(cfg, 1)
+    sc = calibration(cfg)
+    g = run_layer(torch, ssdi8, inp, sc, taps=ALL_TAPS)
+    _check_all(g, inp, sc, cfg, out_dtype=np.float32)
+    # whole-layer oracle (all heads at once) for the global y tolerance
+    ref = oq.ssdi8_forward(inp["x"], inp["dt_raw"], inp["A"], inp["B"], inp["C"], inp["D"],
+                           sc["corr"], sc, chunk=cfg.chunk, want=("y",))
+    assert_close(g["y"], ref["y"], "y (whole layer)")
+
+
+@pytest.mark.parametrize("H,G", [(6, 3), (5, 1), (8, 8)])
+def test_layer_ragged_fp16(torch, ssdi8, H, G):
+    cfg = synth.CONFIGS["mamba2-130m"].scaled(name=f"ragged-{H}-{G}", batch=2, seqlen=768,
+                                              nheads=H, ngroups=G, x_outliers=4)
+    say(f"layer {cfg.name}: B=2 L=768 H={H} G={G} fp16")
+    inp = synth.draw(cfg, 1)
+    sc = calibration(cfg)
+    g = run_layer(torch, ssdi8, inp, sc, taps=ALL_TAPS)
+    _check_all(g, inp, sc, cfg)
+
+
+def _small(name="variant", **kw):
+    base = dict(name=name, batch=2, seqlen=512, nheads=4, ngroups=2, x_outliers=4)
+    base.update(kw)
+    return synth.CONFIGS["mamba2-130m"].scaled(**base)
+
+
+def test_layer_per_head_xs_scale(torch, ssdi8):
+    cfg = _small("per-head", xs_per_head=True)
+    say(f"layer {cfg.name}")
+    inp = synth.draw(cfg, 1)
+    sc = calibration(cfg)
+    assert sc["alpha_Xs"].shape == (4,)
+    g = run_layer(torch, ssdi8, inp, sc, taps=ALL_TAPS)
+    _check_all(g, inp, sc, cfg)
+
+
+def test_layer_per_token_C(torch, ssdi8):
+    cfg = _small("per-token-C")
+    say(f"layer {cfg.name}")
+    inp = synth.draw(cfg, 1)
+    sc = calibration(cfg)
+    g = run_layer(torch, ssdi8, inp, sc, taps=ALL_TAPS, c_per_token=True)
+    for b in range(2):
+        for h in range(4):
+            check_slab(g, inp, sc, b, h, 256, c_scale=g["C_scale"])
+
+
+@pytest.mark.parametrize("shift_round", [True, False])
+def test_layer_floor_or_round_shift_and_init_state(torch, ssdi8, shift_round):
+    cfg = _small("init", seqlen=768)
+    say(f"layer {cfg.name} round={shift_round}")
+    inp = synth.draw(cfg, 1)
+    sc = calibration(cfg)
+    init = np.random.default_rng(5).integers(-127, 128, (2, 4, 64, 128)).astype(np.int8)
+    g = run_layer(torch, ssdi8, inp, sc, taps=ALL_TAPS, shift_round=shift_round, init_q=init)
+    _check_all(g, inp, sc, cfg, shift_round=shift_round, init_q=init)
+
+
+def test_layer_no_softplus_no_skip_no_corr_fp32_out(torch, ssdi8):
+    cfg = _small("raw-dt")
+    say(f"layer {cfg.name}")
+    inp = synth.draw(cfg, 1)
+    inp["dt_raw"] = oq.dt_post(inp["dt_raw"], True)        # pass post-softplus dt
+    sc = calibration(cfg)
+    g = run_layer(torch, ssdi8, inp, sc, taps=ALL_TAPS, dt_softplus=False, use_D=False,
+                  use_corr=False, y_dtype=torch.float32)
+    _check_all(g, inp, sc, cfg, dt_softplus=False, use_D=False, use_corr=False,
+               out_dtype=np.float32)
+
+
+def test_layer_saturating_scales(torch, ssdi8):
+    """Step sizes far too small: every int8 stage saturates; the clamps must match exactly."""
+    cfg = _small("saturate")
+    say(f"layer {cfg.name}")
+    inp = synth.draw(cfg, 1)
+    sc = dict(calibration(cfg))
+    for k, f in (("alpha_Xs", 2000), ("alpha_S", 20000), ("alpha_CB", 1000)):
+        sc[k] = (np.asarray(sc[k]) / f).astype(np.float32)
+    g = run_layer(torch, ssdi8, inp, sc, taps=ALL_TAPS)
+    for name, least in (("xs_q", 0.05), ("state_q", 0.3), ("state_in_q", 0.1), ("cb_q", 0.3)):
+        frac = float(np.mean(np.abs(g[name]) == 127))
+        say(f"  saturated fraction of {name}: {frac:.3f}")
+        assert frac > least, f"{name} saturates only {frac:.3f}"
+    for b in range(2):
+        for h in range(4):
+            check_slab(g, inp, sc, b, h, 256, check_end_to_end=False)
+
+
+# ---------------------------------------------------------------------------- exact cases
+@pytest.mark.parametrize("A_val", [0.0, -1000.0])
+def test_exact_special_cases_on_gpu(torch, ssdi8, A_val):
+    """Integer-valued inputs with unit steps: the int8 path reproduces the fp64 SSD exactly."""
+    say(f"special case A={A_val}")
+    rng = np.random.default_rng(6)
+    Bt, L, H, P, G, N = 1, 512, 2, 64, 1, 128
+    dens = 0.02 if A_val == 0 else 0.3
+
+    def tern(shape, d):
+        return (rng.integers(-1, 2, shape) * (rng.random(shape) < d)).astype(np.float16)
+    inp = {"x": tern((Bt, L, H, P), dens), "B": tern((Bt, L, G, N), dens),
+           "C": tern((Bt, L, G, N), 0.2), "dt_raw": np.ones((Bt, L, H), np.float32),
+           "A": np.full(H, A_val, np.float32), "D": np.ones(H, np.float32)}
+    one = lambda *s: np.ones(s, np.float32)
+    sc = {"alpha_B": one(G), "alpha_C": one(G), "alpha_Xs": one(H, P), "alpha_S": one(H, P),
+          "alpha_CB": one(G), "corr": np.zeros((H, P), np.float32)}
+    ref = oex.ssd_chunked(inp["x"], inp["dt_raw"], inp["A"], inp["B"], inp["C"], inp["D"], 256)
+    assert np.abs(ref["states"]).max() <= 127 and np.abs(ref["entering"]).max() <= 127
+    assert np.abs(ref["final_state"]).max() <= 127 and np.abs(ref["y"]).max() < 2048
+    g = run_layer(torch, ssdi8, inp, sc, taps=ALL_TAPS, dt_softplus=False, y_dtype=torch.float32)
+    assert np.array_equal(g["y"].astype(np.float64), ref["y"])
+    assert np.array_equal(g["final_state_q"].astype(np.float64), ref["final_state"])
+
+
+# ---------------------------------------------------------------------------- ABI behaviour
+def test_determinism_and_resume(torch, ssdi8):
+    cfg = _small("resume", seqlen=1024)
+    say(f"determinism/resume {cfg.name}")
+    inp = synth.draw(cfg, 1)
+    sc = calibration(cfg)
+    a = run_layer(torch, ssdi8, inp, sc, taps=("state_in_q",))
+    b = run_layer(torch, ssdi8, inp, sc, taps=("state_in_q",))
+    for k in a:
+        assert np.array_equal(a[k], b[k]), k
+    half = {k: (v[:, :512] if k in ("x", "dt_raw", "B", "C") else v) for k, v in inp.items()}
+    rest = {k: (v[:, 512:] if k in ("x", "dt_raw", "B", "C") else v) for k, v in inp.items()}
+    h1 = run_layer(torch, ssdi8, half, sc)
+    h2 = run_layer(torch, ssdi8, rest, sc, init_q=h1["final_state_q"])
+    assert np.array_equal(np.concatenate([h1["y"], h2["y"]], axis=1), a["y"])
+    assert np.array_equal(h2["final_state_q"], a["final_state_q"])
+
+
+def test_empty_sequence_returns_initial_state(torch, ssdi8):
+    rng = np.random.default_rng(7)
+    H, P, N, G = 4, 64, 128, 1
+    init = rng.integers(-127, 128, (2, H, P, N)).astype(np.int8)
+    aS = rng.uniform(0.1, 1, (H, P)).astype(np.float32)
+    z = lambda *s, dt=torch.float16: torch.zeros(s, dtype=dt, device="cuda")
+    out = ssdi8.ssd_chunk_scan(
+        z(2, 0, H, P), z(2, 0, H, dt=torch.float32), dev(np.full(H, -1, np.float32), torch),
+        z(2, 0, G, N, dt=torch.int8), z(2, 0, G, N, dt=torch.int8), dev(np.ones(G, np.float32), torch),
+        dev(np.ones(G, np.float32), torch), dev(np.ones((H, P), np.float32), torch),
+        dev(aS, torch), dev(np.ones(G, np.float32), torch), init_state_q=dev(init, torch))
+    torch.cuda.synchronize()
+    assert np.array_equal(out["final_state_q"].cpu().numpy(), init)
+    assert np.array_equal(out["final_state"].cpu().numpy(),
+                          init.astype(np.float32) * aS[None, :, :, None])
+
+
+def test_invalid_arguments_raise(torch, ssdi8):
+    cfg = _small("bad")
+    inp = synth.draw(cfg, 1)
+    x = dev(inp["x"], torch)
+    f = lambda *s: torch.ones(s, dtype=torch.float32, device="cuda")
+    q = torch.zeros((2, 512, 2, 128), dtype=torch.int8, device="cuda")
+    with pytest.raises(ssdi8.SSDi8Error) as e:     # seqlen not a multiple of the chunk
+        ssdi8.ssd_chunk_scan(x[:, :300].contiguous(), f(2, 300, 4), f(4), q[:, :300].contiguous(),
+                             q[:, :300].contiguous(), f(2), f(2), f(4, 64), f(4, 64), f(2))
+    assert e.value.status == ssdi8.ERR_SHAPE
+    with pytest.raises(ssdi8.SSDi8Error) as e:     # unsupported head dim
+        ssdi8.ssd_chunk_scan(x[..., :32].contiguous(), f(2, 512, 4), f(4), q, q, f(2), f(2),
+                             f(4, 32), f(4, 32), f(2))
+    assert e.value.status == ssdi8.ERR_UNSUPPORTED
+    with pytest.raises(ssdi8.SSDi8Error) as e:
+        ssdi8.ssd_chunk_scan(x, f(2, 512, 4), f(4), q, q, f(2), f(2), f(4, 64), f(4, 64), f(2),
+                             decay_shift=0)
+    assert e.value.status == ssdi8.ERR_ARG
