@@ -5,8 +5,9 @@
 // the per-lane K-slice layout of v_mfma_i32_32x32x32_i8, so they feed the MFMA without a
 // transpose.  B and C stay on the group axis (no broadcast to heads).
 //
-// The same workgroup also writes B_q^T of its chunk ([n][j], j contiguous): ChunkState contracts
-// over tokens and needs B with the token axis contiguous, and every head of the group reuses it.
+// A tenth workgroup per chunk writes B_q^T of the chunk ([n][j], j contiguous): ChunkState
+// contracts over tokens and needs B with the token axis contiguous; every head of the group
+// reuses it.
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -15,19 +16,25 @@ namespace ssdi8 {
 namespace {
 
 constexpr int kBS = kN + 16;  // LDS row stride (bytes) of the staged B_q chunk
+constexpr int kTileWGs = 9;   // 36 causal 32x32 tiles = 9 workgroups x 4 waves
+constexpr int kRoles = kTileWGs + 1;
 
+// Work item w -> (b, c, g, role).  Roles 0..8 compute 4 causal tiles each (one per wave); role 9
+// writes B_q^T of the chunk.  The 10 workgroups of one chunk are consecutive work items, so the
+// XCD-aware mapping keeps them on one XCD where the 64 KB of B_q / C_q rows stay in L2.
 __global__ __launch_bounds__(256) void chunk_bmm_kernel(
     const int8_t* __restrict__ Cq, const int8_t* __restrict__ Bq,
     const float* __restrict__ C_scale, int c_per_token, const float* __restrict__ B_scale,
     const float* __restrict__ cb_scale, int8_t* __restrict__ cbq, int32_t* __restrict__ cb32_tap,
     int8_t* __restrict__ bqT, int L, int G, int nc) {
   __shared__ __attribute__((aligned(16))) int8_t s_b[kQ * kBS];
-  __shared__ float s_m[kQ];
 
   const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
   const int w = xcd_remap(blockIdx.x, gridDim.x);
-  const int g = w % G;
-  const int bc = w / G;
+  const int role = w % kRoles;
+  const int bcg = w / kRoles;
+  const int g = bcg % G;
+  const int bc = bcg / G;
   const int c = bc % nc;
   const int b = bc / nc;
   const size_t tok0 = (size_t)b * L + (size_t)c * kQ;
@@ -35,22 +42,16 @@ __global__ __launch_bounds__(256) void chunk_bmm_kernel(
   const int8_t* cbase = Cq + tok0 * rs + (size_t)g * kN;
   const int8_t* bbase = Bq + tok0 * rs + (size_t)g * kN;
 
-  {  // requant multiplier per output row j (per-group, or per-token C step)
-    const float ac = c_per_token ? C_scale[(tok0 + t) * G + g] : C_scale[g];
-    s_m[t] = (float)(((double)ac * (double)B_scale[g]) / (double)cb_scale[g]);
-  }
-  // stage the B_q chunk (256 x 128 bytes), 16 bytes per thread per pass
+  if (role == kTileWGs) {
+    // ---- B_q^T of this chunk ([n][j]): stage the 256 x 128 chunk, read it column-wise
 #pragma unroll
-  for (int it = 0; it < (kQ * kN) / (16 * 256); ++it) {
-    const int idx = it * 256 + t;
-    const int j = idx >> 3, col = (idx & 7) * 16;
-    *reinterpret_cast<uint4*>(s_b + j * kBS + col) =
-        *reinterpret_cast<const uint4*>(bbase + (size_t)j * rs + col);
-  }
-  __syncthreads();
-
-  // B_q^T of this chunk: thread -> state index n (0..127), half of the tokens
-  {
+    for (int it = 0; it < (kQ * kN) / (16 * 256); ++it) {
+      const int idx = it * 256 + t;
+      const int j = idx >> 3, col = (idx & 7) * 16;
+      *reinterpret_cast<uint4*>(s_b + j * kBS + col) =
+          *reinterpret_cast<const uint4*>(bbase + (size_t)j * rs + col);
+    }
+    __syncthreads();
     const int n = t & 127, jh = t >> 7;
     int8_t* dstrow = bqT + ((((size_t)b * nc + c) * G + g) * kN + n) * kQ;
 #pragma unroll
@@ -64,33 +65,43 @@ __global__ __launch_bounds__(256) void chunk_bmm_kernel(
       }
       *reinterpret_cast<uint4*>(dstrow + j0) = make_uint4(wd[0], wd[1], wd[2], wd[3]);
     }
+    return;
   }
 
-  // causal 32x32 tiles (jt >= it): 36 tiles, round-robin over the 4 waves
+  // ---- requant multiplier per output row (per group, or per token row of C), computed before
+  //      the MFMA chain so that no branch separates the last MFMA from the reads of its result
+  __shared__ float s_m[kQ];
+  {
+    const float ac = c_per_token ? C_scale[(tok0 + t) * G + g] : C_scale[g];
+    s_m[t] = (float)(((double)ac * (double)B_scale[g]) / (double)cb_scale[g]);
+  }
+  __syncthreads();
+
+  // ---- one causal 32x32 tile per wave
+  int jt = 0, it = role * 4 + wv;
+  while (it > jt) { it -= jt + 1; ++jt; }
+  const int8_t* arow = cbase + (size_t)(jt * 32 + (lane & 31)) * rs + 16 * (lane >> 5);
+  const int8_t* brow = bbase + (size_t)(it * 32 + (lane & 31)) * rs + 16 * (lane >> 5);
+  v4i a[4], bb[4];
+#pragma unroll
+  for (int ks = 0; ks < kN / 32; ++ks) {
+    a[ks] = *reinterpret_cast<const v4i*>(arow + 32 * ks);
+    bb[ks] = *reinterpret_cast<const v4i*>(brow + 32 * ks);
+  }
+  v16i acc = {};
+#pragma unroll
+  for (int ks = 0; ks < kN / 32; ++ks)
+    acc = __builtin_amdgcn_mfma_i32_32x32x32_i8(a[ks], bb[ks], acc, 0, 0, 0);
   const size_t obase = (((size_t)b * nc + c) * G + g) * (size_t)kQ * kQ;
-  for (int tile = wv; tile < 36; tile += 4) {
-    int jt = 0, acc_t = tile;
-    while (acc_t > jt) { acc_t -= jt + 1; ++jt; }
-    const int it = acc_t;
-    v16i acc = {};
-    const int8_t* arow = cbase + (size_t)(jt * 32 + (lane & 31)) * rs;
-    const int8_t* brow = s_b + (it * 32 + (lane & 31)) * kBS;
+  const int i = it * 32 + (lane & 31);
 #pragma unroll
-    for (int ks = 0; ks < kN / 32; ++ks) {
-      const int kof = ks * 32 + 16 * (lane >> 5);
-      const v4i a = *reinterpret_cast<const v4i*>(arow + kof);
-      const v4i bb = *reinterpret_cast<const v4i*>(brow + kof);
-      acc = __builtin_amdgcn_mfma_i32_32x32x32_i8(a, bb, acc, 0, 0, 0);
-    }
-    const int i = it * 32 + (lane & 31);
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int j = jt * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-      const bool keep = i <= j;
-      const int v = keep ? acc[r] : 0;
-      cbq[obase + (size_t)j * kQ + i] = (int8_t)(keep ? requant_i8(v, s_m[j]) : 0);
-      if (cb32_tap) cb32_tap[obase + (size_t)j * kQ + i] = v;
-    }
+  for (int r = 0; r < 16; ++r) {
+    const int j = jt * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+    const float m = s_m[j];
+    const bool keep = i <= j;
+    const int v = keep ? acc[r] : 0;
+    cbq[obase + (size_t)j * kQ + i] = (int8_t)(keep ? requant_i8(v, m) : 0);
+    if (cb32_tap) cb32_tap[obase + (size_t)j * kQ + i] = v;
   }
 }
 
@@ -100,7 +111,7 @@ hipError_t launch_chunk_bmm(const LayerDims& d, const int8_t* Cq, const int8_t* 
                             const float* C_scale, int c_per_token, const float* B_scale,
                             const float* cb_scale, int8_t* cbq, int32_t* cb32_tap, int8_t* bqT,
                             hipStream_t st) {
-  const int64_t nwork = (int64_t)d.batch * d.nchunks * d.ngroups;
+  const int64_t nwork = (int64_t)d.batch * d.nchunks * d.ngroups * kRoles;
   if (nwork == 0) return hipSuccess;
   hipLaunchKernelGGL(chunk_bmm_kernel, dim3((unsigned)nwork), dim3(256), 0, st, Cq, Bq, C_scale,
                      c_per_token, B_scale, cb_scale, cbq, cb32_tap, bqT, d.seqlen, d.ngroups,

@@ -22,22 +22,29 @@ namespace {
 
 constexpr int kXS = kQ + 16;  // LDS row stride (bytes) of X_q^T
 
-template <typename XT>
-__device__ __forceinline__ void load_pair(const XT* p, float& a, float& b);
-
-template <>
-__device__ __forceinline__ void load_pair<_Float16>(const _Float16* p, float& a, float& b) {
-  const uint32_t v = *reinterpret_cast<const uint32_t*>(p);
-  a = (float)__builtin_bit_cast(_Float16, (uint16_t)(v & 0xffffu));
-  b = (float)__builtin_bit_cast(_Float16, (uint16_t)(v >> 16));
-}
-
-template <>
-__device__ __forceinline__ void load_pair<float>(const float* p, float& a, float& b) {
-  const float2 v = *reinterpret_cast<const float2*>(p);
-  a = v.x;
-  b = v.y;
-}
+// Two adjacent channels of one token row, loaded raw (the loads are issued before the decay table
+// they are scaled by is ready) and unpacked to fp32 later.
+template <typename XT> struct Pair;
+template <> struct Pair<_Float16> {
+  typedef uint32_t raw;
+  static __device__ __forceinline__ raw load(const _Float16* p) {
+    return *reinterpret_cast<const uint32_t*>(p);
+  }
+  static __device__ __forceinline__ float lo(raw v) {
+    return (float)__builtin_bit_cast(_Float16, (uint16_t)(v & 0xffffu));
+  }
+  static __device__ __forceinline__ float hi(raw v) {
+    return (float)__builtin_bit_cast(_Float16, (uint16_t)(v >> 16));
+  }
+};
+template <> struct Pair<float> {
+  typedef float2 raw;
+  static __device__ __forceinline__ raw load(const float* p) {
+    return *reinterpret_cast<const float2*>(p);
+  }
+  static __device__ __forceinline__ float lo(raw v) { return v.x; }
+  static __device__ __forceinline__ float hi(raw v) { return v.y; }
+};
 
 template <typename XT>
 __global__ __launch_bounds__(256) void chunk_state_kernel(
@@ -63,6 +70,16 @@ __global__ __launch_bounds__(256) void chunk_state_kernel(
   const size_t tok0 = (size_t)b * L + (size_t)c * kQ;
   const size_t HP = (size_t)H * kP;
 
+  // ---- issue the x tile loads first (thread: channel pair (p0, p0+1), tokens
+  //      [32 jb, 32 jb + 32)); they overlap the ChunkCumsum below
+  const int pp = t & 31, jb = t >> 5, p0 = 2 * pp;
+  typename Pair<XT>::raw xr[32];
+  {
+    const XT* xb = x + (tok0 + (size_t)jb * 32) * HP + (size_t)h * kP + p0;
+#pragma unroll
+    for (int r = 0; r < 32; ++r) xr[r] = Pair<XT>::load(xb + (size_t)r * HP);
+  }
+
   // ---- ChunkCumsum: token t
   float dtv = dt[(tok0 + t) * H + h];
   if (dt_softplus) dtv = softplus_f32(dtv);
@@ -80,31 +97,21 @@ __global__ __launch_bounds__(256) void chunk_state_kernel(
   if (t == 0) qd[((size_t)b * H + h) * nc + c] = (int16_t)rint(exp(last) * (double)(1 << shift));
   __syncthreads();
 
-  // ---- X_scaled -> X_q, written transposed to LDS.  Thread: channel pair (p0, p0+1), tokens
-  //      [32 jb, 32 jb + 32).
+  // ---- X_scaled -> X_q, written transposed to LDS ([p][j], tokens contiguous)
   {
-    const int pp = t & 31, jb = t >> 5, p0 = 2 * pp;
     const float inv0 = s_inv[p0], inv1 = s_inv[p0 + 1];
     uint32_t w0[8], w1[8];
+    int qa[32], qb[32];
+#pragma unroll
+    for (int r = 0; r < 32; ++r) {
+      const float lut = s_lut[jb * 32 + r];
+      qa[r] = quant_i8(lut * Pair<XT>::lo(xr[r]), inv0);
+      qb[r] = quant_i8(lut * Pair<XT>::hi(xr[r]), inv1);
+    }
 #pragma unroll
     for (int r4 = 0; r4 < 8; ++r4) {
-      int qa[4], qb[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int j = jb * 32 + r4 * 4 + u;
-        const size_t off = (tok0 + j) * HP + (size_t)h * kP + p0;
-        float xa, xb;
-        load_pair<XT>(x + off, xa, xb);
-        const float lut = s_lut[j];
-        qa[u] = quant_i8(lut * xa, inv0);
-        qb[u] = quant_i8(lut * xb, inv1);
-        if (xq_tap) {
-          *reinterpret_cast<uint16_t*>(xq_tap + off) =
-              (uint16_t)((qa[u] & 0xff) | ((qb[u] & 0xff) << 8));
-        }
-      }
-      w0[r4] = pack4_i8(qa[0], qa[1], qa[2], qa[3]);
-      w1[r4] = pack4_i8(qb[0], qb[1], qb[2], qb[3]);
+      w0[r4] = pack4_i8(qa[4 * r4], qa[4 * r4 + 1], qa[4 * r4 + 2], qa[4 * r4 + 3]);
+      w1[r4] = pack4_i8(qb[4 * r4], qb[4 * r4 + 1], qb[4 * r4 + 2], qb[4 * r4 + 3]);
     }
     int8_t* r0 = s_xq + p0 * kXS + jb * 32;
     int8_t* r1 = r0 + kXS;
@@ -112,6 +119,13 @@ __global__ __launch_bounds__(256) void chunk_state_kernel(
     *reinterpret_cast<uint4*>(r0 + 16) = make_uint4(w0[4], w0[5], w0[6], w0[7]);
     *reinterpret_cast<uint4*>(r1) = make_uint4(w1[0], w1[1], w1[2], w1[3]);
     *reinterpret_cast<uint4*>(r1 + 16) = make_uint4(w1[4], w1[5], w1[6], w1[7]);
+    if (xq_tap) {
+      int8_t* tb = xq_tap + (tok0 + (size_t)jb * 32) * HP + (size_t)h * kP + p0;
+#pragma unroll
+      for (int r = 0; r < 32; ++r)
+        *reinterpret_cast<uint16_t*>(tb + (size_t)r * HP) =
+            (uint16_t)((qa[r] & 0xff) | ((qb[r] & 0xff) << 8));
+    }
   }
   __syncthreads();
 

@@ -50,6 +50,20 @@ def rel_errors(y_gpu, y_ref) -> Tuple[float, float]:
     return maxabs, rel
 
 
+def assert_equal(gpu, ref, what: str) -> None:
+    """Bit-exact comparison that names the stage and shows where it differs."""
+    gpu = np.asarray(gpu)
+    ref = np.asarray(ref)
+    assert gpu.shape == ref.shape, f"{what}: shape {gpu.shape} vs {ref.shape}"
+    bad = gpu != ref
+    if bad.any():
+        idx = np.argwhere(bad)
+        first = [(tuple(int(v) for v in i), gpu[tuple(i)].item(), ref[tuple(i)].item())
+                 for i in idx[:8]]
+        raise AssertionError(f"{what} mismatch: {int(bad.sum())} of {bad.size} differ; "
+                             f"first (index, gpu, oracle): {first}")
+
+
 def assert_close(y_gpu, y_ref, what="y") -> Tuple[float, float]:
     maxabs, rel = rel_errors(y_gpu, y_ref)
     say(f"  {what}: max|d|/max|ref| = {maxabs:.3e}  relL2 = {rel:.3e}")
@@ -140,31 +154,31 @@ def check_slab(g: Dict[str, np.ndarray], inp, sc, b: int, h: int, cfg_chunk: int
             nc = xq.shape[0] // Q
             s32 = oq._int_matmul(np.swapaxes(xq.reshape(nc, Q, -1), 1, 2),
                                  Bq_g.reshape(nc, Q, -1))
-            assert np.array_equal(g["state_i32"][b, :, h], s32), "State_INT32 mismatch"
+            assert_equal(g["state_i32"][b, :, h], s32, "State_INT32")
             if "state_q" in g:
                 ms = oq.multiplier(s["alpha_xs"], s["alpha_B"], s["alpha_S"])
                 sq = oq.requant(g["state_i32"][b, :, h], ms[None, :, None])
-                assert np.array_equal(g["state_q"][b, :, h], sq), "State_INT8 mismatch"
+                assert_equal(g["state_q"][b, :, h], sq, "State_INT8")
     # StatePassing, stage-isolated on the GPU's S_q and q_d
     if "state_in_q" in g and "state_q" in g and "decay_q" in g:
         init = None if init_q is None else init_q[b, h]
         pin, fin = oq.state_pass(g["state_q"][b, :, h], g["decay_q"][b, h], init, k, shift_round)
-        assert np.array_equal(g["state_in_q"][b, :, h], pin), "P_in mismatch"
-        assert np.array_equal(g["final_state_q"][b, h], fin), "final_q mismatch"
+        assert_equal(g["state_in_q"][b, :, h], pin, "P_in")
+        assert_equal(g["final_state_q"][b, h], fin, "final_q")
         fs = fin.astype(np.float32) * np.asarray(sc["alpha_S"], np.float32)[h][:, None]
-        assert np.array_equal(g["final_state"][b, h], fs), "final fp32 state mismatch"
+        assert_equal(g["final_state"][b, h], fs, "final fp32 state")
     # ChunkBMM, stage-isolated on the GPU's B_q, C_q
     if "cb_i32" in g:
         cb = oq.chunk_bmm(Cq_g, Bq_g, s["alpha_C"], s["alpha_B"], s["alpha_CB"], Q)
-        assert np.array_equal(g["cb_i32"][b, :, gi], cb["CB32"]), "CB_INT32 mismatch"
+        assert_equal(g["cb_i32"][b, :, gi], cb["CB32"], "CB_INT32")
         if "cb_q" in g:
-            assert np.array_equal(g["cb_q"][b, :, gi], cb["CBq"]), "CB_INT8 mismatch"
+            assert_equal(g["cb_q"][b, :, gi], cb["CBq"], "CB_INT8")
     # ChunkScan1 product, stage-isolated on the GPU's C_q and P_in
     if "scan1_i32" in g and "state_in_q" in g:
         nc = Cq_g.shape[0] // Q
         y1 = oq._int_matmul(Cq_g.reshape(nc, Q, -1),
                             np.swapaxes(g["state_in_q"][b, :, h], 1, 2)).reshape(-1, g["state_in_q"].shape[3])
-        assert np.array_equal(g["scan1_i32"][b, :, h], y1), "ChunkScan1 INT32 mismatch"
+        assert_equal(g["scan1_i32"][b, :, h], y1, "ChunkScan1 INT32")
     D_h = np.float32(inp["D"][h]) if use_D else np.float32(0)
     corr_h = np.asarray(sc["corr"], np.float32)[h] if use_corr else np.zeros(inp["x"].shape[3], np.float32)
     # output, stage-isolated: oracle ChunkScan on the GPU's P_in and CB_q
@@ -179,12 +193,12 @@ def check_slab(g: Dict[str, np.ndarray], inp, sc, b: int, h: int, cfg_chunk: int
                                 np.asarray(sc["alpha_B"], np.float32)[gi:gi + 1])
         if c_scale is not None:       # per-token C steps: the oracle derives its own
             Co, aCo = oq.quantize_act(inp["C"][b:b + 1, :, gi:gi + 1], "token")
-            assert np.array_equal(aCo[0, :, 0], s["alpha_C"]), "per-token C steps differ"
+            assert_equal(s["alpha_C"], aCo[0, :, 0], "per-token C steps")
         else:
             Co, _ = oq.quantize_act(inp["C"][b:b + 1, :, gi:gi + 1], "group",
                                     np.asarray(sc["alpha_C"], np.float32)[gi:gi + 1])
-        assert np.array_equal(Bo[0, :, 0], Bq_g), "B_q mismatch"
-        assert np.array_equal(Co[0, :, 0], Cq_g), "C_q mismatch"
+        assert_equal(Bq_g, Bo[0, :, 0], "B_q")
+        assert_equal(Cq_g, Co[0, :, 0], "C_q")
         ref = oq.ssdi8_slab(inp["x"][b, :, h], dt32, A_h, Bo[0, :, 0], Co[0, :, 0], D_h, corr_h,
                             s, Q, k, shift_round, init, out_dtype)
         assert_close(g["y"][b, :, h], ref["y"], f"y[b={b},h={h}] (end-to-end)")

@@ -6,7 +6,7 @@ max|dy|/max|y| <= 1e-2 and relative L2 <= 1e-3."""
 import numpy as np
 import pytest
 
-from helpers import assert_close, calibration, check_slab, dev, run_layer, say
+from helpers import assert_close, assert_equal, calibration, check_slab, dev, run_layer, say
 from oracle import exact as oex
 from oracle import int8 as oq
 from paper_2608_21952_amd import synth
