@@ -92,6 +92,11 @@ def main():
     ap.add_argument("--workload", default="mamba2-130m")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget-s", type=float, default=15.0)
+    ap.add_argument("--eager", action="store_true",
+                    help="time eager launches instead of replays of one captured HIP graph")
+    ap.add_argument("--copy-probe-mb", type=int, default=0,
+                    help="after the timed region, run one plain device-to-device copy of this "
+                         "many MiB (a known-size reference for HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: --gpus {args.gpus} is not supported by this build "
@@ -142,15 +147,38 @@ def main():
     for _ in range(W):
         step()
     torch.cuda.synchronize()
+    graph = None
+    if not args.eager:
+        # one step captured as a HIP graph on a side stream; the timed region replays it
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            step()
+        torch.cuda.current_stream().wait_stream(side)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step()
+        for _ in range(W):
+            graph.replay()
+        torch.cuda.synchronize()
     t0 = torch.cuda.Event(enable_timing=True)
     t1 = torch.cuda.Event(enable_timing=True)
     t0.record()
     for k in range(K):
-        step(k)
+        if graph is not None:
+            graph.replay()
+        else:
+            step(k)
     t1.record()
     torch.cuda.synchronize()
     total_ms = t0.elapsed_time(t1)
     ms_step = total_ms / K
+    if graph is not None:
+        # per-kernel durations: K eager steps with HIP events recorded on the launch stream
+        # between the kernels (the kernels are the same; only launch gaps differ)
+        for k in range(K):
+            step(k)
+        torch.cuda.synchronize()
     # per-module averages over the timed steps (events on the launch stream)
     names = ("quantize_B", "quantize_C") + MODULES
     per = {n: 0.0 for n in names}
@@ -188,9 +216,17 @@ def main():
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4),
                      "traffic": traffic, "algorithmic_bytes": abytes[dom],
                      "avg_us": round(per[dom] * 1e3, 2)},
+        "timing": "HIP graph replay" if graph is not None else "eager launches",
         "layer_hbm_frac": round(layer_min_bytes(cfg) / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "stages": stages,
     }
+    if args.copy_probe_mb > 0:
+        n = args.copy_probe_mb << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a bounded sample ...", file=sys.stderr,
               flush=True)

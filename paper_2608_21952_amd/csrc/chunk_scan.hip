@@ -17,7 +17,8 @@
 //
 // Work split: wave w owns the j-blocks {w, 7-w} (1+w + 8-w = 9 causal block pairs per wave).
 // x is staged once in LDS as x^T [p][i] (fp16, tokens contiguous = the Scan2 MFMA K-slice) and
-// also serves the D skip term; the fp16 output leaves through an LDS stage as 128-byte rows.
+// in row order [j][p] for the D skip term; the fp16 output is written over the x rows and leaves
+// through that stage as 128-byte rows.
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -64,15 +65,39 @@ __global__ __launch_bounds__(256, 2) void chunk_scan_kernel(
     const float* __restrict__ cb_scale, const float* __restrict__ state_scale,
     const float* __restrict__ Dv, const float* __restrict__ corr, int dt_softplus,
     YT* __restrict__ y, int32_t* __restrict__ y1_tap, int L, int H, int G, int nc) {
-  __shared__ __attribute__((aligned(16))) uint8_t s_xT[kP * kXTS];
-  __shared__ __attribute__((aligned(16))) uint8_t s_y[sizeof(YT) == 2 ? kQ * kYS : 16];
-  __shared__ double s_cs[kQ];
-  __shared__ float s_u[kQ];     // a_CB dt_i exp(r_I - cs_i)
-  __shared__ float s_dtcb[kQ];  // a_CB dt_i
-  __shared__ float s_vp[kQ];    // exp(cs_j - r_{J-1})
-  __shared__ float s_eoff[kQ];  // a_C(j) exp(cs_j)
-  __shared__ float s_R[8][8];   // exp(r_a - r_b), b <= a
-  __shared__ double s_scan[4];
+  constexpr bool kHalfX = sizeof(XT) == 2;
+  // One LDS block with the small per-token tables first, so that their offsets fit the 16-bit
+  // ds offset field (separate __shared__ arrays may be placed large-first).
+  struct __attribute__((aligned(16))) Smem {
+    // Column tables of the ChunkScan2 weights, interleaved as (w, -128 w) pairs so that an int8
+    // weight q, converted as the unsigned byte q + 128, gives fl32(q w) = fma(q + 128, w, -128 w)
+    // exactly (the fma forms (q + 128) w - 128 w = q w before its one rounding).
+    float2 u[kQ];        // a_CB dt_i exp(r_I - cs_i)
+    float2 dtcb[kQ];     // a_CB dt_i
+    float csr[kQ];       // cs_i - r_{I-1} (r_{-1} = 0), fp32
+    float eoff[kQ];      // a_C(j) exp(cs_j)
+    float R[8][8];       // exp(r_a - r_b), b <= a
+    float aS[kP];
+    float cr[kP];
+    double cs[kQ];
+    double scan[4];
+    // x^T [p][i] fp16 (the ChunkScan2 MFMA operand) and, for fp16 x, x in row order [j][p] (the
+    // D skip operand), which the epilogue overwrites in place with y as the output stage.
+    uint8_t xT[kP * kXTS];
+    uint8_t xr[kHalfX ? kQ * kYS : 16];
+  };
+  __shared__ Smem sm;
+  float2* s_u = sm.u;
+  float2* s_dtcb = sm.dtcb;
+  float* s_csr = sm.csr;
+  float* s_eoff = sm.eoff;
+  float (*s_R)[8] = sm.R;
+  float* s_aS = sm.aS;
+  float* s_cr = sm.cr;
+  double* s_cs = sm.cs;
+  double* s_scan = sm.scan;
+  uint8_t* s_xT = sm.xT;
+  uint8_t* s_xr = sm.xr;
 
   const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
   const int w = xcd_remap(blockIdx.x, gridDim.x);
@@ -100,13 +125,18 @@ __global__ __launch_bounds__(256, 2) void chunk_scan_kernel(
   const float dA = dtv * A[h];
   const double cs = block_scan_f64_256((double)dA, s_scan);
   s_cs[t] = cs;
+  if (t < kP) {
+    s_aS[t] = state_scale[h * kP + t];
+    s_cr[t] = corr ? corr[h * kP + t] : 0.0f;
+  }
   __syncthreads();
   {
     const int blk = t >> 5;
     const float dtcb = aCB * dtv;
-    s_dtcb[t] = dtcb;
-    s_u[t] = dtcb * expf((float)(s_cs[blk * 32 + 31] - cs));
-    s_vp[t] = blk ? expf((float)(cs - s_cs[blk * 32 - 1])) : 1.0f;
+    const float u = dtcb * expf((float)(s_cs[blk * 32 + 31] - cs));
+    s_dtcb[t] = make_float2(dtcb, -128.0f * dtcb);
+    s_u[t] = make_float2(u, -128.0f * u);
+    s_csr[t] = (float)(blk ? cs - s_cs[blk * 32 - 1] : cs);
     const float ac = c_per_token ? C_scale[(tok0 + t) * G + g] : C_scale[g];
     s_eoff[t] = ac * expf((float)cs);
     if (t < 64) {
@@ -114,7 +144,7 @@ __global__ __launch_bounds__(256, 2) void chunk_scan_kernel(
       s_R[ra][rb] = (rb <= ra) ? expf((float)(s_cs[ra * 32 + 31] - s_cs[rb * 32 + 31])) : 0.0f;
     }
   }
-  // ---- x^T [p][i] as fp16 in LDS (tokens contiguous = the ChunkScan2 MFMA K-slice)
+  // ---- x^T [p][i] (fp16) and x rows [j][p] (fp16 input) in LDS
   {
     uint8_t* r0 = s_xT + p0 * kXTS + jb * 64;
     uint8_t* r1 = r0 + kXTS;
@@ -130,22 +160,27 @@ __global__ __launch_bounds__(256, 2) void chunk_scan_kernel(
       *reinterpret_cast<uint4*>(r0 + 16 * q) = make_uint4(a[0], a[1], a[2], a[3]);
       *reinterpret_cast<uint4*>(r1 + 16 * q) = make_uint4(bb[0], bb[1], bb[2], bb[3]);
     }
+    if constexpr (kHalfX) {
+#pragma unroll
+      for (int r = 0; r < 32; ++r)
+        *reinterpret_cast<uint32_t*>(s_xr + (jb * 32 + r) * kYS + p0 * 2) = (uint32_t)xr[r];
+    }
   }
   __syncthreads();
 
+  // Both products are formed transposed (MFMA rows = channels p, columns = tokens j), so each
+  // lane owns one token row j and runs of 4 consecutive channels: the epilogue needs one row
+  // factor per lane and moves 8-byte vectors.  Lane l: j = 32 jt + (l % 32); accumulator
+  // register r holds channel p = 32 pt + 8 (r / 4) + 4 (l / 32) + r % 4.
   const int8_t* pbase = pin + (((size_t)b * nc + c) * H + h) * (size_t)kP * kN;
   const int8_t* cbbase = cbq + (((size_t)b * nc + c) * G + g) * (size_t)kQ * kQ;
   const int pc = lane & 31, half = lane >> 5;
-  const float aS0 = state_scale[h * kP + pc];
-  const float aS1 = state_scale[h * kP + 32 + pc];
-  const float cr0 = corr ? corr[h * kP + pc] : 0.0f;
-  const float cr1 = corr ? corr[h * kP + 32 + pc] : 0.0f;
   const float Dh = Dv ? Dv[h] : 0.0f;
 
   for (int q2 = 0; q2 < 2; ++q2) {
     const int jt = q2 ? 7 - wv : wv;
     const int jrow = jt * 32 + pc;
-    // -- Scan1: int8 MFMA over n (C_q rows against the entering state rows)
+    // -- Scan1: Y1^T = P_in . C_q^T, int8 MFMA over n
     v16i yi0 = {}, yi1 = {};
     {
       const int8_t* crow = Cq + ((tok0 + jrow) * G + g) * kN + 16 * half;
@@ -160,16 +195,16 @@ __global__ __launch_bounds__(256, 2) void chunk_scan_kernel(
       }
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) {
-        yi0 = __builtin_amdgcn_mfma_i32_32x32x32_i8(a[ks], b0[ks], yi0, 0, 0, 0);
-        yi1 = __builtin_amdgcn_mfma_i32_32x32x32_i8(a[ks], b1[ks], yi1, 0, 0, 0);
+        yi0 = __builtin_amdgcn_mfma_i32_32x32x32_i8(b0[ks], a[ks], yi0, 0, 0, 0);
+        yi1 = __builtin_amdgcn_mfma_i32_32x32x32_i8(b1[ks], a[ks], yi1, 0, 0, 0);
       }
     }
-    // -- Scan2: fp16 MFMA over the causal source tokens i, CB_q of block it+1 prefetched
+    // -- Scan2: y_diag^T = x^T . W^T, fp16 MFMA over the causal source tokens i; CB_q of
+    //    block it+1 is prefetched while block it is built
     v16f yd0 = {}, yd1 = {};
     {
       const int8_t* cbrow = cbbase + (size_t)jrow * kQ + 8 * half;
-      const double csj = s_cs[jrow];
-      const float vpj = s_vp[jrow];
+      const float csrj = s_csr[jrow];
       uint2 cur0 = *reinterpret_cast<const uint2*>(cbrow);
       uint2 cur1 = *reinterpret_cast<const uint2*>(cbrow + 16);
       for (int it = 0; it <= jt; ++it) {
@@ -178,68 +213,105 @@ __global__ __launch_bounds__(256, 2) void chunk_scan_kernel(
           nx0 = *reinterpret_cast<const uint2*>(cbrow + (it + 1) * 32);
           nx1 = *reinterpret_cast<const uint2*>(cbrow + (it + 1) * 32 + 16);
         }
-        const float vj = (it < jt) ? vpj * s_R[jt - 1][it] : 0.0f;
+        // row factor of an off-diagonal block: exp(cs_j - r_{J-1}) exp(r_{J-1} - r_I)
+        const float vj = (it < jt) ? __expf(csrj) * s_R[jt - 1][it] : 0.0f;
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
           const uint2 cb8 = ks ? cur1 : cur0;
           const int i0 = it * 32 + ks * 16 + 8 * half;
-          v8h wf;
+          // int8 weights as unsigned bytes (q + 128), 4 per dword
+          const uint32_t ub0 = cb8.x ^ 0x80808080u, ub1 = cb8.y ^ 0x80808080u;
+          float wv[8];
           if (it < jt) {
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
-              const int cbv = sext8(e < 4 ? cb8.x : cb8.y, e & 3);
-              wf[e] = (_Float16)(((float)cbv * s_u[i0 + e]) * vj);
+              const float2 uu = s_u[i0 + e];
+              const float qb = (float)(((e < 4 ? ub0 : ub1) >> (8 * (e & 3))) & 0xffu);
+              wv[e] = __builtin_fmaf(qb, uu.x, uu.y) * vj;
             }
           } else {
+            // diagonal block: exp per element; the clamp keeps the masked (i > j) entries finite
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
               const int i = i0 + e;
-              const int cbv = sext8(e < 4 ? cb8.x : cb8.y, e & 3);
-              float wv_ = 0.0f;
-              if (i <= jrow) wv_ = ((float)cbv * s_dtcb[i]) * __expf((float)(csj - s_cs[i]));
-              wf[e] = (_Float16)wv_;
+              const float2 dd = s_dtcb[i];
+              const float qb = (float)(((e < 4 ? ub0 : ub1) >> (8 * (e & 3))) & 0xffu);
+              const float ex = __expf(__builtin_fminf(csrj - s_csr[i], 0.0f));
+              const float v = __builtin_fmaf(qb, dd.x, dd.y) * ex;
+              wv[e] = (i <= jrow) ? v : 0.0f;
             }
           }
-          const v8h xb0 = *reinterpret_cast<const v8h*>(s_xT + pc * kXTS + i0 * 2);
-          const v8h xb1 = *reinterpret_cast<const v8h*>(s_xT + (32 + pc) * kXTS + i0 * 2);
-          yd0 = __builtin_amdgcn_mfma_f32_32x32x16_f16(wf, xb0, yd0, 0, 0, 0);
-          yd1 = __builtin_amdgcn_mfma_f32_32x32x16_f16(wf, xb1, yd1, 0, 0, 0);
+          v8h wf;
+#pragma unroll
+          for (int e = 0; e < 8; e += 2) {
+            typedef float f2_t __attribute__((ext_vector_type(2)));
+            typedef _Float16 h2_t __attribute__((ext_vector_type(2)));
+            const f2_t pr = {wv[e], wv[e + 1]};
+            const h2_t hh = __builtin_convertvector(pr, h2_t);
+            wf[e] = hh.x;
+            wf[e + 1] = hh.y;
+          }
+          const v8h xa0 = *reinterpret_cast<const v8h*>(s_xT + pc * kXTS + i0 * 2);
+          const v8h xa1 = *reinterpret_cast<const v8h*>(s_xT + (32 + pc) * kXTS + i0 * 2);
+          yd0 = __builtin_amdgcn_mfma_f32_32x32x16_f16(xa0, wf, yd0, 0, 0, 0);
+          yd1 = __builtin_amdgcn_mfma_f32_32x32x16_f16(xa1, wf, yd1, 0, 0, 0);
         }
         cur0 = nx0;
         cur1 = nx1;
       }
     }
-    // -- epilogue for this j-block: y = y_off + y_diag + D x + corr
+    // -- epilogue of token row jrow: y = Y1 a_C exp(cs_j) a_S[p] + y_diag + D x + corr[p]
+    const float eo = s_eoff[jrow];
+    const size_t orow = (tok0 + jrow) * HP + (size_t)h * kP;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int j = jt * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-      const float eo = s_eoff[j];
-      const size_t orow = (tok0 + j) * HP + (size_t)h * kP;
-      float x0, x1;
-      if constexpr (sizeof(XT) == 2) {
-        x0 = (float)*reinterpret_cast<const _Float16*>(s_xT + pc * kXTS + j * 2);
-        x1 = (float)*reinterpret_cast<const _Float16*>(s_xT + (32 + pc) * kXTS + j * 2);
-      } else {
-        x0 = (float)x[orow + pc];
-        x1 = (float)x[orow + 32 + pc];
-      }
-      const float v0 = ((float)yi0[r] * eo) * aS0 + yd0[r] + Dh * x0 + cr0;
-      const float v1 = ((float)yi1[r] * eo) * aS1 + yd1[r] + Dh * x1 + cr1;
-      if (y1_tap) {
-        y1_tap[orow + pc] = yi0[r];
-        y1_tap[orow + 32 + pc] = yi1[r];
-      }
-      if constexpr (sizeof(YT) == 4) {
-        y[orow + pc] = v0;
-        y[orow + 32 + pc] = v1;
-      } else {
-        *reinterpret_cast<_Float16*>(s_y + j * kYS + pc * 2) = (_Float16)v0;
-        *reinterpret_cast<_Float16*>(s_y + j * kYS + (32 + pc) * 2) = (_Float16)v1;
+    for (int pt = 0; pt < 2; ++pt) {
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4) {
+        const int pb = pt * 32 + 8 * g4 + 4 * half;
+        const float4 as4 = *reinterpret_cast<const float4*>(s_aS + pb);
+        const float4 cr4 = *reinterpret_cast<const float4*>(s_cr + pb);
+        float xv[4];
+        if constexpr (kHalfX) {
+          const uint2 xw = *reinterpret_cast<const uint2*>(s_xr + jrow * kYS + pb * 2);
+          xv[0] = (float)__builtin_bit_cast(_Float16, (uint16_t)(xw.x & 0xffffu));
+          xv[1] = (float)__builtin_bit_cast(_Float16, (uint16_t)(xw.x >> 16));
+          xv[2] = (float)__builtin_bit_cast(_Float16, (uint16_t)(xw.y & 0xffffu));
+          xv[3] = (float)__builtin_bit_cast(_Float16, (uint16_t)(xw.y >> 16));
+        } else {
+          const float4 xf = *reinterpret_cast<const float4*>(x + orow + pb);
+          xv[0] = xf.x; xv[1] = xf.y; xv[2] = xf.z; xv[3] = xf.w;
+        }
+        const float asv[4] = {as4.x, as4.y, as4.z, as4.w};
+        const float crv[4] = {cr4.x, cr4.y, cr4.z, cr4.w};
+        float v[4];
+        int yi[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int r = 4 * g4 + q;
+          yi[q] = pt ? yi1[r] : yi0[r];
+          const float yd = pt ? yd1[r] : yd0[r];
+          v[q] = (((float)yi[q] * eo) * asv[q] + yd) + Dh * xv[q] + crv[q];
+        }
+        if (y1_tap)
+          *reinterpret_cast<int4*>(y1_tap + orow + pb) = make_int4(yi[0], yi[1], yi[2], yi[3]);
+        if constexpr (sizeof(YT) == 4) {
+          *reinterpret_cast<float4*>(y + orow + pb) = make_float4(v[0], v[1], v[2], v[3]);
+        } else {
+          uint2 o;
+          o.x = (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)v[0]) |
+                ((uint32_t)__builtin_bit_cast(uint16_t, (_Float16)v[1]) << 16);
+          o.y = (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)v[2]) |
+                ((uint32_t)__builtin_bit_cast(uint16_t, (_Float16)v[3]) << 16);
+          if constexpr (kHalfX)
+            *reinterpret_cast<uint2*>(s_xr + jrow * kYS + pb * 2) = o;   // in place over x
+          else
+            *reinterpret_cast<uint2*>(y + orow + pb) = o;
+        }
       }
     }
   }
 
-  if constexpr (sizeof(YT) == 2) {
+  if constexpr (sizeof(YT) == 2 && kHalfX) {
     __syncthreads();
 #pragma unroll
     for (int k = 0; k < (kQ * kP * 2) / (16 * 256); ++k) {
@@ -247,7 +319,7 @@ __global__ __launch_bounds__(256, 2) void chunk_scan_kernel(
       const int j = idx >> 3, col = idx & 7;
       *reinterpret_cast<uint4*>(reinterpret_cast<uint8_t*>(y) +
                                 ((tok0 + j) * HP + (size_t)h * kP) * 2 + col * 16) =
-          *reinterpret_cast<const uint4*>(s_y + j * kYS + col * 16);
+          *reinterpret_cast<const uint4*>(s_xr + j * kYS + col * 16);
     }
   }
 }

@@ -286,3 +286,34 @@ def test_invalid_arguments_raise(torch, ssdi8):
         ssdi8.ssd_chunk_scan(x, f(2, 512, 4), f(4), q, q, f(2), f(2), f(4, 64), f(4, 64), f(2),
                              decay_shift=0)
     assert e.value.status == ssdi8.ERR_ARG
+
+
+def test_graph_replay_matches_eager(torch, ssdi8):
+    """One layer captured as a HIP graph: every replay (with eager work and synchronisations in
+    between) reproduces the eager outputs bit for bit."""
+    cfg = _small("graph", seqlen=768)
+    say(f"graph replay {cfg.name}")
+    inp = synth.draw(cfg, 1)
+    sc = calibration(cfg)
+    eager = run_layer(torch, ssdi8, inp, sc, taps=("state_in_q", "cb_q"))
+    x, dt = dev(inp["x"], torch), dev(inp["dt_raw"], torch)
+    Bf, Cf = dev(inp["B"], torch), dev(inp["C"], torch)
+    layer = ssdi8.SSDi8Layer(inp["A"], inp["D"], sc["corr"], sc, device="cuda")
+    y = torch.empty_like(x)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        layer(x, dt, Bf, Cf, y=y)
+    torch.cuda.current_stream().wait_stream(side)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        out = layer(x, dt, Bf, Cf, y=y, taps=("state_in_q", "cb_q"))
+    for rep in range(4):
+        y.zero_()
+        out["state_in_q"].zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(y.cpu().numpy(), eager["y"]), f"replay {rep}: y differs"
+        assert np.array_equal(out["state_in_q"].cpu().numpy(), eager["state_in_q"]), rep
+        assert np.array_equal(out["final_state_q"].cpu().numpy(), eager["final_state_q"]), rep
