@@ -50,6 +50,23 @@ def layer_min_bytes(cfg):
     return 2 * T * H * P * sx + T * H * 4 + 2 * T * G * N * sx + B * H * P * N * 5
 
 
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 FETCH_SIZE / WRITE_SIZE
+    summary (each counter scaled by what it reads for a plain copy of known size), or None when
+    there is none or the kernel's source changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload}.json")
+    src = os.path.join(ROOT, "paper_2608_21952_amd", "csrc", f"{kernel}.hip")
+    if not os.path.exists(path) or not os.path.exists(src):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    with open(src, "rb") as f:
+        if hashlib.sha256(f.read()).hexdigest() != rec.get("source_sha256"):
+            return None
+    return rec.get("bytes_per_launch")
+
+
 def cpu_baseline(cfg, inp, sc, budget_s: float):
     """The CPU oracle as it stands, timed on a bounded sample: batch element 0, the first
     `nh` heads (all chunks), nh sized from a one-head pilot to about `budget_s` seconds."""
@@ -149,7 +166,7 @@ def main():
     torch.cuda.synchronize()
     graph = None
     if not args.eager:
-        # one step captured as a HIP graph on a side stream; the timed region replays it
+        # one step captured as a HIP graph on a side stream; the timed region replays it K times
         side = torch.cuda.Stream()
         side.wait_stream(torch.cuda.current_stream())
         with torch.cuda.stream(side):
@@ -174,8 +191,8 @@ def main():
     total_ms = t0.elapsed_time(t1)
     ms_step = total_ms / K
     if graph is not None:
-        # per-kernel durations: K eager steps with HIP events recorded on the launch stream
-        # between the kernels (the kernels are the same; only launch gaps differ)
+        # per-kernel durations: K eager steps right after, with HIP events recorded on the
+        # launch stream between the kernels (same kernels; an event record adds ~1-3 us)
         for k in range(K):
             step(k)
         torch.cuda.synchronize()
@@ -199,11 +216,7 @@ def main():
     ach = abytes[dom] / (per[dom] * 1e-3) / 1e9
     tokens = cfg.batch * cfg.seqlen
     value = tokens / (ms_step * 1e-3)
-    traffic_path = os.path.join(ROOT, "profiles", f"traffic_{dom}_{cfg.name}.json")
-    traffic = None
-    if os.path.exists(traffic_path):
-        with open(traffic_path) as f:
-            traffic = json.load(f).get("bytes_per_launch")
+    traffic = measured_traffic(dom, cfg.name)
     result = {
         "metric": "INT8 SSD chunk-scan tokens/s per layer",
         "value": value, "unit": "tokens/s", "n_gpus": 1, "steps": K, "warmup": W,
@@ -216,7 +229,8 @@ def main():
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4),
                      "traffic": traffic, "algorithmic_bytes": abytes[dom],
                      "avg_us": round(per[dom] * 1e3, 2)},
-        "timing": "HIP graph replay" if graph is not None else "eager launches",
+        "timing": ("K replays of one captured HIP graph; per-kernel times from K eager steps "
+                   "bracketed by HIP events" if graph is not None else "eager launches"),
         "layer_hbm_frac": round(layer_min_bytes(cfg) / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "stages": stages,
     }

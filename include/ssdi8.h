@@ -152,7 +152,8 @@ typedef struct {
   void* workspace; size_t workspace_bytes;
   /* Optional per-module timing: NULL, or 5 hipEvent_t handles created by the caller; they are
      recorded on `stream` before ChunkBMM, before ChunkState, before StatePassing, before
-     ChunkScan and after ChunkScan (the module breakdown of the paper's latency figures). */
+     ChunkScan and after ChunkScan (the module breakdown of the paper's latency figures).
+     Leave NULL when the call is captured into a HIP graph. */
   void* const* stage_events;
 } ssdi8_scan_args;
 

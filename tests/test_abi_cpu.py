@@ -1,0 +1,169 @@
+"""The C ABI on the CPU (no GPU needed): the library loads and exports every function that
+include/ssdi8.h declares, the binding's structs match the C layout, and every argument error
+is reported by status code before anything is launched."""
+import ctypes
+import os
+import re
+import subprocess
+import sys
+import tempfile
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ssdi8.h")
+
+
+@pytest.fixture(scope="module")
+def ssdi8():
+    from paper_2608_21952_amd import ssdi8 as s
+    if not os.path.exists(s.LIB_PATH):
+        from paper_2608_21952_amd.build import build
+        build()
+    s.lib()
+    return s
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[\w\s\*]+?\b(ssdi8_\w+)\s*\(", text, re.M)))
+
+
+def test_every_declared_function_is_exported(ssdi8):
+    names = declared_functions()
+    assert {"ssdi8_quantize_act", "ssdi8_state_pass", "ssdi8_ssd_chunk_scan",
+            "ssdi8_ssd_workspace_size", "ssdi8_status_string", "ssdi8_version"} <= set(names)
+    out = subprocess.run(["nm", "-D", "--defined-only", ssdi8.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\bT (ssdi8_\w+)", out))
+    assert set(names) <= exported, set(names) - exported
+    for n in names:
+        getattr(ssdi8.lib(), n)
+
+
+def test_structs_match_the_header(ssdi8, tmp_path):
+    fields = [f[0] for f in ssdi8.ScanArgs._fields_]
+    src = tmp_path / "layout.c"
+    lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "ssdi8.h"', 'int main(void) {',
+             'printf("%zu %zu\\n", sizeof(ssdi8_scan_args), sizeof(ssdi8_dims));']
+    for f in fields:
+        lines.append(f'printf("%zu\\n", offsetof(ssdi8_scan_args, {f}));')
+    lines.append("return 0; }")
+    src.write_text("\n".join(lines))
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-std=c11", "-I", os.path.join(ROOT, "include"), str(src), "-o",
+                    str(exe)], check=True)
+    vals = [int(v) for v in subprocess.run([str(exe)], capture_output=True, text=True,
+                                           check=True).stdout.split()]
+    assert vals[0] == ctypes.sizeof(ssdi8.ScanArgs)
+    assert vals[1] == ctypes.sizeof(ssdi8.Dims)
+    for f, off in zip(fields, vals[2:]):
+        assert getattr(ssdi8.ScanArgs, f).offset == off, f
+
+
+def test_status_strings_and_version(ssdi8):
+    for s in range(8):
+        assert ssdi8.status_string(s)
+    assert "unknown" in ssdi8.status_string(99)
+    assert re.match(r"\d+\.\d+\.\d+", ssdi8.version())
+
+
+def test_workspace_size(ssdi8):
+    d = ssdi8.dims(4, 4096, 80, 1)
+    B, L, H, P, G, N, Q = 4, 4096, 80, 64, 1, 128, 256
+    c = L // Q
+    need = B * L * G * N + 2 * B * c * H * P * N + B * c * G * Q * Q + B * H * c * 2
+    ws = ssdi8.workspace_size(d)
+    assert need <= ws <= need + 5 * 256
+    assert ssdi8.workspace_size(ssdi8.dims(1, 300, 4, 1)) == 0          # L % chunk
+    assert ssdi8.workspace_size(ssdi8.dims(1, 512, 6, 4)) == 0          # H % G
+    assert ssdi8.workspace_size(ssdi8.dims(1, 512, 4, 1, headdim=32)) == 0
+
+
+A16 = 0x10000          # fake, 16-byte aligned device addresses: never dereferenced on error paths
+
+
+def _scan_args(ssdi8, **over):
+    a = ssdi8.ScanArgs()
+    for f in ("x", "dt", "A", "Bq", "Cq", "B_scale", "C_scale", "xs_scale", "state_scale",
+              "cb_scale", "y", "workspace"):
+        setattr(a, f, A16)
+    a.x_dtype = a.y_dtype = ssdi8.F16
+    a.decay_shift, a.shift_round, a.dt_softplus = 7, 1, 1
+    a.workspace_bytes = 1 << 40
+    for k, v in over.items():
+        setattr(a, k, v)
+    return a
+
+
+def _scan(ssdi8, d, a):
+    return ssdi8.lib().ssdi8_ssd_chunk_scan(ctypes.byref(d), ctypes.byref(a), None)
+
+
+@pytest.mark.parametrize("field", ["x", "dt", "A", "Bq", "Cq", "B_scale", "C_scale", "xs_scale",
+                                   "state_scale", "cb_scale", "y"])
+def test_scan_null_pointer(ssdi8, field):
+    assert _scan(ssdi8, ssdi8.dims(1, 512, 4, 1), _scan_args(ssdi8, **{field: None})) == \
+        ssdi8.ERR_NULL
+
+
+def test_scan_argument_errors(ssdi8):
+    L = ssdi8.lib()
+    ok = ssdi8.dims(1, 512, 4, 2)
+    assert L.ssdi8_ssd_chunk_scan(None, ctypes.byref(_scan_args(ssdi8)), None) == ssdi8.ERR_NULL
+    assert L.ssdi8_ssd_chunk_scan(ctypes.byref(ok), None, None) == ssdi8.ERR_NULL
+    assert _scan(ssdi8, ssdi8.dims(1, 300, 4, 2), _scan_args(ssdi8)) == ssdi8.ERR_SHAPE
+    assert _scan(ssdi8, ssdi8.dims(1, 512, 6, 4), _scan_args(ssdi8)) == ssdi8.ERR_SHAPE
+    assert _scan(ssdi8, ssdi8.dims(-1, 512, 4, 2), _scan_args(ssdi8)) == ssdi8.ERR_SHAPE
+    assert _scan(ssdi8, ssdi8.dims(1, 512, 4, 2, headdim=128), _scan_args(ssdi8)) == \
+        ssdi8.ERR_UNSUPPORTED
+    assert _scan(ssdi8, ssdi8.dims(1, 512, 4, 2, dstate=64), _scan_args(ssdi8)) == \
+        ssdi8.ERR_UNSUPPORTED
+    assert _scan(ssdi8, ssdi8.dims(1, 1024, 4, 2, chunk=128), _scan_args(ssdi8)) == \
+        ssdi8.ERR_UNSUPPORTED
+    assert _scan(ssdi8, ok, _scan_args(ssdi8, decay_shift=0)) == ssdi8.ERR_ARG
+    assert _scan(ssdi8, ok, _scan_args(ssdi8, decay_shift=15)) == ssdi8.ERR_ARG
+    assert _scan(ssdi8, ok, _scan_args(ssdi8, x_dtype=5)) == ssdi8.ERR_ARG
+    assert _scan(ssdi8, ok, _scan_args(ssdi8, x=A16 + 8)) == ssdi8.ERR_ALIGN
+    assert _scan(ssdi8, ok, _scan_args(ssdi8, state_q=A16 + 4)) == ssdi8.ERR_ALIGN
+    assert _scan(ssdi8, ok, _scan_args(ssdi8, workspace_bytes=16)) == ssdi8.ERR_WORKSPACE
+    assert _scan(ssdi8, ok, _scan_args(ssdi8, workspace=None)) == ssdi8.ERR_WORKSPACE
+    ev = (ctypes.c_void_p * 5)(A16, A16, None, A16, A16)
+    assert _scan(ssdi8, ok, _scan_args(ssdi8, stage_events=ctypes.cast(ev, ctypes.c_void_p))) == \
+        ssdi8.ERR_NULL
+
+
+def test_quantize_argument_errors(ssdi8):
+    q = ssdi8.lib().ssdi8_quantize_act
+    assert q(A16, 1, 2, 8, 1, 128, 1, None, 0, A16, None) == ssdi8.ERR_NULL
+    assert q(None, 1, 2, 8, 1, 128, 1, A16, 0, A16, None) == ssdi8.ERR_NULL
+    assert q(A16, 3, 2, 8, 1, 128, 1, A16, 0, A16, None) == ssdi8.ERR_ARG
+    assert q(A16, 1, 2, 8, 1, 128, 7, A16, 0, A16, None) == ssdi8.ERR_ARG
+    assert q(A16, 1, -2, 8, 1, 128, 1, A16, 0, A16, None) == ssdi8.ERR_SHAPE
+    assert q(A16, 1, 2, 8, 0, 128, 1, A16, 0, A16, None) == ssdi8.ERR_SHAPE
+    assert q(A16 + 2, 1, 2, 8, 1, 128, 1, A16, 0, A16, None) == ssdi8.ERR_ALIGN
+    assert q(A16, 1, 2, 8, 64, 256, 2, A16, 1, A16, None) == ssdi8.ERR_UNSUPPORTED
+
+
+def test_state_pass_argument_errors(ssdi8):
+    sp = ssdi8.lib().ssdi8_state_pass
+    args = dict(sq=A16, qd=A16, shift=7, rnd=1, init=None, pin=A16, fq=None, fs=None, ss=None)
+
+    def call(**kw):
+        a = dict(args)
+        a.update(kw)
+        return sp(a["sq"], a["qd"], a["shift"], a["rnd"], a["init"], a["pin"], a["fq"],
+                  a["fs"], a["ss"], 1, 4, 2, 64, 128, None)
+    assert call(sq=None) == ssdi8.ERR_NULL
+    assert call(pin=None) == ssdi8.ERR_NULL
+    assert call(fs=A16) == ssdi8.ERR_NULL            # fp32 state needs the state steps
+    assert call(shift=0) == ssdi8.ERR_ARG
+    assert call(qd=A16 + 1) == ssdi8.ERR_ALIGN
+    assert sp(A16, A16, 7, 1, None, A16, None, None, None, 1, 4, 2, 64, 126, None) == \
+        ssdi8.ERR_UNSUPPORTED
+
+
+def test_bench_refuses_more_than_one_gpu():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2 and "one GPU" in r.stderr
