@@ -5,6 +5,7 @@
 #include <hip/hip_runtime.h>
 
 #include "common.hpp"
+#include "frag.hpp"
 #include "launch.hpp"
 
 namespace {
@@ -19,11 +20,12 @@ bool aligned16_or_null(const void* p) { return p == nullptr || aligned16(p); }
 size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 struct Plan {
-  size_t bqT, sq, pin, cbq, qd, total;
+  size_t bqT, cq, sq, pin, cbq, qd, total;
 };
 
-// Workspace regions (256-byte aligned): B_q^T chunks, chunk-local int8 states, entering int8
-// states, int8 C.B^T, int16 Q(Decay).
+// Workspace regions (256-byte aligned), the int8 ones in the MFMA fragment order of frag.hpp:
+// B_q^T and C_q per chunk, chunk-local and entering int8 states, the causal blocks of the int8
+// C.B^T; then the int16 Q(Decay).
 Plan plan_workspace(const ssdi8_dims* d) {
   const size_t B = (size_t)d->batch, L = (size_t)d->seqlen, H = (size_t)d->nheads;
   const size_t P = (size_t)d->headdim, G = (size_t)d->ngroups, N = (size_t)d->dstate;
@@ -31,9 +33,11 @@ Plan plan_workspace(const ssdi8_dims* d) {
   Plan p;
   size_t off = 0;
   p.bqT = off; off = round_up(off + B * L * G * N, 256);
+  p.cq = off;  off = round_up(off + B * L * G * N, 256);
   p.sq = off;  off = round_up(off + B * nc * H * P * N, 256);
   p.pin = off; off = round_up(off + B * nc * H * P * N, 256);
-  p.cbq = off; off = round_up(off + B * nc * G * Q * Q, 256);
+  p.cbq = off; off = round_up(off + B * nc * G * (size_t)ssdi8::frag::kCbChunkBytes, 256);
+  (void)Q;
   p.qd = off;  off = round_up(off + B * H * nc * sizeof(int16_t), 256);
   p.total = off;
   return p;
@@ -120,8 +124,8 @@ ssdi8_status ssdi8_state_pass(const int8_t* state_q, const int16_t* decay_q, int
     return SSDI8_ERR_ALIGN;
   hipError_t e = ssdi8::launch_state_pass(batch, nchunks, nheads, headdim * dstate, headdim,
                                           state_q, decay_q, shift, shift_round, init_q,
-                                          state_in_q, final_q, final_state, state_scale,
-                                          (hipStream_t)stream);
+                                          state_in_q, nullptr, final_q, final_state, state_scale,
+                                          0, (hipStream_t)stream);
   return e == hipSuccess ? SSDI8_OK : SSDI8_ERR_HIP;
 }
 
@@ -167,8 +171,9 @@ ssdi8_status ssdi8_ssd_chunk_scan(const ssdi8_dims* d, const ssdi8_scan_args* a,
     if (d->batch > 0 && (a->final_state_q || a->final_state)) {
       hipError_t e = ssdi8::launch_state_pass(d->batch, 0, d->nheads, elems, d->headdim,
                                               nullptr, nullptr, a->decay_shift, a->shift_round,
-                                              a->init_state_q, nullptr, a->final_state_q,
-                                              a->final_state, a->state_scale, st);
+                                              a->init_state_q, nullptr, nullptr,
+                                              a->final_state_q, a->final_state, a->state_scale,
+                                              0, st);
       if (e != hipSuccess) return SSDI8_ERR_HIP;
     }
     return SSDI8_OK;
@@ -176,9 +181,10 @@ ssdi8_status ssdi8_ssd_chunk_scan(const ssdi8_dims* d, const ssdi8_scan_args* a,
 
   char* ws = static_cast<char*>(a->workspace);
   int8_t* bqT = reinterpret_cast<int8_t*>(ws + plan.bqT);
-  int8_t* sq = a->state_q ? a->state_q : reinterpret_cast<int8_t*>(ws + plan.sq);
-  int8_t* pin = a->state_in_q ? a->state_in_q : reinterpret_cast<int8_t*>(ws + plan.pin);
-  int8_t* cbq = a->cb_q ? a->cb_q : reinterpret_cast<int8_t*>(ws + plan.cbq);
+  int8_t* cq = reinterpret_cast<int8_t*>(ws + plan.cq);
+  int8_t* sq = reinterpret_cast<int8_t*>(ws + plan.sq);
+  int8_t* pin = reinterpret_cast<int8_t*>(ws + plan.pin);
+  int8_t* cbq = reinterpret_cast<int8_t*>(ws + plan.cbq);
   int16_t* qd = a->decay_q ? a->decay_q : reinterpret_cast<int16_t*>(ws + plan.qd);
 
   auto mark = [&](int i) -> bool {
@@ -187,17 +193,19 @@ ssdi8_status ssdi8_ssd_chunk_scan(const ssdi8_dims* d, const ssdi8_scan_args* a,
   };
   if (!mark(0)) return SSDI8_ERR_HIP;
   hipError_t e = ssdi8::launch_chunk_bmm(ld, a->Cq, a->Bq, a->C_scale, a->c_per_token,
-                                         a->B_scale, a->cb_scale, cbq, a->cb_i32, bqT, st);
+                                         a->B_scale, a->cb_scale, cbq, a->cb_q, a->cb_i32, bqT,
+                                         cq, st);
   if (e != hipSuccess || !mark(1)) return SSDI8_ERR_HIP;
   e = ssdi8::launch_chunk_state(ld, a->x, a->x_dtype, a->dt, a->dt_softplus, a->A, bqT,
                                 a->B_scale, a->xs_scale, a->xs_per_head, a->state_scale,
-                                a->decay_shift, sq, qd, a->xs_q, a->state_i32, st);
+                                a->decay_shift, sq, qd, a->xs_q, a->state_q, a->state_i32, st);
   if (e != hipSuccess || !mark(2)) return SSDI8_ERR_HIP;
   e = ssdi8::launch_state_pass(d->batch, ld.nchunks, d->nheads, elems, d->headdim, sq, qd,
                                a->decay_shift, a->shift_round, a->init_state_q, pin,
-                               a->final_state_q, a->final_state, a->state_scale, st);
+                               a->state_in_q, a->final_state_q, a->final_state, a->state_scale,
+                               (int)d->dstate, st);
   if (e != hipSuccess || !mark(3)) return SSDI8_ERR_HIP;
-  e = ssdi8::launch_chunk_scan(ld, a->x, a->x_dtype, a->dt, a->dt_softplus, a->A, a->Cq,
+  e = ssdi8::launch_chunk_scan(ld, a->x, a->x_dtype, a->dt, a->dt_softplus, a->A, cq,
                                a->C_scale, a->c_per_token, pin, cbq, a->cb_scale, a->state_scale,
                                a->D, a->corr, a->y, a->y_dtype, a->scan1_i32, st);
   if (e != hipSuccess || !mark(4)) return SSDI8_ERR_HIP;

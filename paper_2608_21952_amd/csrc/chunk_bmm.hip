@@ -5,10 +5,15 @@
 // the per-lane K-slice layout of v_mfma_i32_32x32x32_i8, so they feed the MFMA without a
 // transpose.  B and C stay on the group axis (no broadcast to heads).
 //
-// A tenth workgroup per chunk writes B_q^T of the chunk ([n][j], j contiguous): ChunkState
-// contracts over tokens and needs B with the token axis contiguous; every head of the group
-// reuses it.
+// Outputs for the later kernels are written in MFMA fragment order (frag.hpp): a wave reads
+// each operand fragment as one contiguous 1 KB run.
+//   CB_q   the 36 causal 32x32 blocks of the chunk, as ChunkScan2 B-operand fragments
+//   C_q    a fragment-order copy of the chunk's C_q rows (ChunkScan1 operand), written by the
+//          waves of the i = 0 blocks, which hold exactly those fragments in registers
+//   B_q^T  written by a tenth workgroup per chunk: ChunkState contracts over tokens and needs B
+//          with the token axis as the K-slice; every head of the group reuses it.
 #include "common.hpp"
+#include "frag.hpp"
 #include "launch.hpp"
 
 namespace ssdi8 {
@@ -25,8 +30,9 @@ constexpr int kRoles = kTileWGs + 1;
 __global__ __launch_bounds__(256) void chunk_bmm_kernel(
     const int8_t* __restrict__ Cq, const int8_t* __restrict__ Bq,
     const float* __restrict__ C_scale, int c_per_token, const float* __restrict__ B_scale,
-    const float* __restrict__ cb_scale, int8_t* __restrict__ cbq, int32_t* __restrict__ cb32_tap,
-    int8_t* __restrict__ bqT, int L, int G, int nc) {
+    const float* __restrict__ cb_scale, int8_t* __restrict__ cbq_frag,
+    int8_t* __restrict__ cbq_tap, int32_t* __restrict__ cb32_tap, int8_t* __restrict__ bqT_frag,
+    int8_t* __restrict__ cq_frag, int L, int G, int nc) {
   __shared__ __attribute__((aligned(16))) int8_t s_b[kQ * kBS];
 
   const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
@@ -41,6 +47,7 @@ __global__ __launch_bounds__(256) void chunk_bmm_kernel(
   const size_t rs = (size_t)G * kN;  // token stride of B_q / C_q rows
   const int8_t* cbase = Cq + tok0 * rs + (size_t)g * kN;
   const int8_t* bbase = Bq + tok0 * rs + (size_t)g * kN;
+  const size_t cg = ((size_t)b * nc + c) * G + g;   // chunk-group index
 
   if (role == kTileWGs) {
     // ---- B_q^T of this chunk ([n][j]): stage the 256 x 128 chunk, read it column-wise
@@ -53,7 +60,7 @@ __global__ __launch_bounds__(256) void chunk_bmm_kernel(
     }
     __syncthreads();
     const int n = t & 127, jh = t >> 7;
-    int8_t* dstrow = bqT + ((((size_t)b * nc + c) * G + g) * kN + n) * kQ;
+    int8_t* dst = bqT_frag + cg * (size_t)kN * kQ;
 #pragma unroll
     for (int blk = 0; blk < kQ / 32; ++blk) {
       const int j0 = jh * (kQ / 2) + blk * 16;
@@ -63,7 +70,8 @@ __global__ __launch_bounds__(256) void chunk_bmm_kernel(
         wd[u] = pack4_i8(s_b[(j0 + 4 * u) * kBS + n], s_b[(j0 + 4 * u + 1) * kBS + n],
                          s_b[(j0 + 4 * u + 2) * kBS + n], s_b[(j0 + 4 * u + 3) * kBS + n]);
       }
-      *reinterpret_cast<uint4*>(dstrow + j0) = make_uint4(wd[0], wd[1], wd[2], wd[3]);
+      *reinterpret_cast<uint4*>(dst + frag::kslice_offset(n, j0, kQ)) =
+          make_uint4(wd[0], wd[1], wd[2], wd[3]);
     }
     return;
   }
@@ -88,34 +96,58 @@ __global__ __launch_bounds__(256) void chunk_bmm_kernel(
     a[ks] = *reinterpret_cast<const v4i*>(arow + 32 * ks);
     bb[ks] = *reinterpret_cast<const v4i*>(brow + 32 * ks);
   }
+  if (it == 0) {
+    // the C_q rows of block jt, in ChunkScan1 fragment order (before the MFMA chain, so that no
+    // branch separates the last MFMA from the reads of its result)
+    int8_t* cdst = cq_frag + cg * (size_t)kQ * kN;
+#pragma unroll
+    for (int ks = 0; ks < kN / 32; ++ks)
+      *reinterpret_cast<v4i*>(cdst + frag::kslice_offset(jt * 32 + (lane & 31),
+                                                         32 * ks + 16 * (lane >> 5), kN)) = a[ks];
+  }
   v16i acc = {};
 #pragma unroll
   for (int ks = 0; ks < kN / 32; ++ks)
     acc = __builtin_amdgcn_mfma_i32_32x32x32_i8(a[ks], bb[ks], acc, 0, 0, 0);
-  const size_t obase = (((size_t)b * nc + c) * G + g) * (size_t)kQ * kQ;
+  // requantize into this wave's 1 KB stage in CB fragment order, then one 16-byte store per lane
+  int8_t* stage = s_b + wv * 1024;
+  const size_t obase = cg * (size_t)kQ * kQ;
   const int i = it * 32 + (lane & 31);
+  int v[16], q[16];
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
-    const int j = jt * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-    const float m = s_m[j];
-    const bool keep = i <= j;
-    const int v = keep ? acc[r] : 0;
-    cbq[obase + (size_t)j * kQ + i] = (int8_t)(keep ? requant_i8(v, m) : 0);
-    if (cb32_tap) cb32_tap[obase + (size_t)j * kQ + i] = v;
+    const int jj = 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+    const bool keep = i <= jt * 32 + jj;
+    v[r] = keep ? acc[r] : 0;
+    q[r] = keep ? requant_i8(v[r], s_m[jt * 32 + jj]) : 0;
+    stage[frag::cb_inblock(jj, lane & 31)] = (int8_t)q[r];
   }
+  if (cbq_tap || cb32_tap) {   // row-major debug copies
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const size_t o = obase + (size_t)(jt * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)) * kQ + i;
+      if (cbq_tap) cbq_tap[o] = (int8_t)q[r];
+      if (cb32_tap) cb32_tap[o] = v[r];
+    }
+  }
+  __syncthreads();
+  *reinterpret_cast<uint4*>(cbq_frag + cg * (size_t)frag::kCbChunkBytes +
+                            (size_t)frag::cb_block(jt, it) * 1024 + lane * 16) =
+      *reinterpret_cast<const uint4*>(stage + lane * 16);
 }
 
 }  // namespace
 
 hipError_t launch_chunk_bmm(const LayerDims& d, const int8_t* Cq, const int8_t* Bq,
                             const float* C_scale, int c_per_token, const float* B_scale,
-                            const float* cb_scale, int8_t* cbq, int32_t* cb32_tap, int8_t* bqT,
+                            const float* cb_scale, int8_t* cbq_frag, int8_t* cbq_tap,
+                            int32_t* cb32_tap, int8_t* bqT_frag, int8_t* cq_frag,
                             hipStream_t st) {
   const int64_t nwork = (int64_t)d.batch * d.nchunks * d.ngroups * kRoles;
   if (nwork == 0) return hipSuccess;
   hipLaunchKernelGGL(chunk_bmm_kernel, dim3((unsigned)nwork), dim3(256), 0, st, Cq, Bq, C_scale,
-                     c_per_token, B_scale, cb_scale, cbq, cb32_tap, bqT, d.seqlen, d.ngroups,
-                     d.nchunks);
+                     c_per_token, B_scale, cb_scale, cbq_frag, cbq_tap, cb32_tap, bqT_frag,
+                     cq_frag, d.seqlen, d.ngroups, d.nchunks);
   return hipGetLastError();
 }
 

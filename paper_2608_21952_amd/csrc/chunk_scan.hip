@@ -13,13 +13,18 @@
 // (J, I the blocks of j, i; every factor <= 1, so nothing overflows and an underflow only
 // happens where the true weight underflows).  The row / block / column factors are computed
 // once per chunk (fp32 exp of differences formed from the fp64 sums), so an off-diagonal weight
-// costs two fp32 products and no exp; only the 8 diagonal blocks evaluate exp per element.
+// costs two fp32 products and no exp.  A diagonal block splits the same way about r_{J-1}
+// (exp(cs_j - r_{J-1}) exp(r_{J-1} - cs_i)) when its span r_{J-1} - r_J is small enough for the
+// second factor to stay finite; otherwise it evaluates exp per element.
 //
 // Work split: wave w owns the j-blocks {w, 7-w} (1+w + 8-w = 9 causal block pairs per wave).
-// x is staged once in LDS as x^T [p][i] (fp16, tokens contiguous = the Scan2 MFMA K-slice) and
-// in row order [j][p] for the D skip term; the fp16 output is written over the x rows and leaves
-// through that stage as 128-byte rows.
+// x is staged once in LDS as x^T [p][i] (fp16, tokens contiguous = the Scan2 MFMA K-slice); the
+// D skip term reads it back per token, and the fp16 output leaves through the same bytes as whole
+// 128-byte rows.  C_q, P_in and CB_q arrive in MFMA fragment order (frag.hpp), so every operand
+// load is one contiguous 1 KB run per wave.  About 45 KB of LDS and at most 168 VGPRs per lane
+// let three workgroups share a CU.
 #include "common.hpp"
+#include "frag.hpp"
 #include "launch.hpp"
 
 namespace ssdi8 {
@@ -27,7 +32,10 @@ namespace ssdi8 {
 namespace {
 
 constexpr int kXTS = kQ * 2 + 16;   // bytes per channel row of x^T (fp16)
-constexpr int kYS = kP * 2 + 16;    // bytes per token row of the staged fp16 output
+static_assert(kP * kXTS >= kQ * kP * 2, "the fp16 output stage reuses the x^T bytes");
+// A diagonal block whose decay span r_{J-1} - r_J stays below this bound forms its weights as
+// (a_CB dt_i exp(-(cs_i - r_{J-1}))) * exp(cs_j - r_{J-1}) without overflow in fp32.
+constexpr float kDiagSpan = 64.0f;
 
 // Two adjacent channels of one token row, loaded raw and converted to fp16 for the MFMA.
 template <typename XT> struct Pair;
@@ -52,20 +60,24 @@ template <> struct Pair<float> {
   }
 };
 
-// fp32 softplus (the output path only needs dt to fp32 accuracy).
+// softplus to a few fp32 ulps (the output path only needs dt to fp32 accuracy): log1p(e) for
+// e = exp(v) as log(u) * e / (u - 1) with u = fl(1 + e), which cancels the rounding of u.
 __device__ __forceinline__ float softplus_fast(float v) {
-  return v > 20.0f ? v : log1pf(expf(v));
+  const float e = __expf(v);
+  const float u = 1.0f + e;
+  const float d = u - 1.0f;
+  const float lp = (d == 0.0f) ? e : __logf(u) * (e / d);
+  return v > 20.0f ? v : lp;
 }
 
 template <typename XT, typename YT>
-__global__ __launch_bounds__(256, 2) void chunk_scan_kernel(
+__global__ __launch_bounds__(256, 3) void chunk_scan_kernel(
     const XT* __restrict__ x, const float* __restrict__ dt, const float* __restrict__ A,
-    const int8_t* __restrict__ Cq, const float* __restrict__ C_scale, int c_per_token,
+    const int8_t* __restrict__ cq_frag, const float* __restrict__ C_scale, int c_per_token,
     const int8_t* __restrict__ pin, const int8_t* __restrict__ cbq,
     const float* __restrict__ cb_scale, const float* __restrict__ state_scale,
     const float* __restrict__ Dv, const float* __restrict__ corr, int dt_softplus,
     YT* __restrict__ y, int32_t* __restrict__ y1_tap, int L, int H, int G, int nc) {
-  constexpr bool kHalfX = sizeof(XT) == 2;
   // One LDS block with the small per-token tables first, so that their offsets fit the 16-bit
   // ds offset field (separate __shared__ arrays may be placed large-first).
   struct __attribute__((aligned(16))) Smem {
@@ -74,6 +86,7 @@ __global__ __launch_bounds__(256, 2) void chunk_scan_kernel(
     // exactly (the fma forms (q + 128) w - 128 w = q w before its one rounding).
     float2 u[kQ];        // a_CB dt_i exp(r_I - cs_i)
     float2 dtcb[kQ];     // a_CB dt_i
+    float2 ud[kQ];       // a_CB dt_i exp(r_{I-1} - cs_i), clamped (diagonal blocks of small span)
     float csr[kQ];       // cs_i - r_{I-1} (r_{-1} = 0), fp32
     float eoff[kQ];      // a_C(j) exp(cs_j)
     float R[8][8];       // exp(r_a - r_b), b <= a
@@ -81,14 +94,14 @@ __global__ __launch_bounds__(256, 2) void chunk_scan_kernel(
     float cr[kP];
     double cs[kQ];
     double scan[4];
-    // x^T [p][i] fp16 (the ChunkScan2 MFMA operand) and, for fp16 x, x in row order [j][p] (the
-    // D skip operand), which the epilogue overwrites in place with y as the output stage.
+    // x^T [p][i] fp16: the ChunkScan2 MFMA operand and, for fp16 x, the D skip operand; then
+    // the stage of the fp16 output (256 rows of 128 bytes).
     uint8_t xT[kP * kXTS];
-    uint8_t xr[kHalfX ? kQ * kYS : 16];
   };
   __shared__ Smem sm;
   float2* s_u = sm.u;
   float2* s_dtcb = sm.dtcb;
+  float2* s_ud = sm.ud;
   float* s_csr = sm.csr;
   float* s_eoff = sm.eoff;
   float (*s_R)[8] = sm.R;
@@ -97,9 +110,9 @@ __global__ __launch_bounds__(256, 2) void chunk_scan_kernel(
   double* s_cs = sm.cs;
   double* s_scan = sm.scan;
   uint8_t* s_xT = sm.xT;
-  uint8_t* s_xr = sm.xr;
 
-  const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
+  const int t = threadIdx.x, lane = t & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(t >> 6);   // wave-uniform, so block loops are scalar
   const int w = xcd_remap(blockIdx.x, gridDim.x);
   const int h = w % H;
   const int bc = w / H;
@@ -136,7 +149,10 @@ __global__ __launch_bounds__(256, 2) void chunk_scan_kernel(
     const float u = dtcb * expf((float)(s_cs[blk * 32 + 31] - cs));
     s_dtcb[t] = make_float2(dtcb, -128.0f * dtcb);
     s_u[t] = make_float2(u, -128.0f * u);
-    s_csr[t] = (float)(blk ? cs - s_cs[blk * 32 - 1] : cs);
+    const float csr = (float)(blk ? cs - s_cs[blk * 32 - 1] : cs);
+    s_csr[t] = csr;
+    const float ud = dtcb * expf(__builtin_fminf(-csr, 2.0f * kDiagSpan));
+    s_ud[t] = make_float2(ud, -128.0f * ud);
     const float ac = c_per_token ? C_scale[(tok0 + t) * G + g] : C_scale[g];
     s_eoff[t] = ac * expf((float)cs);
     if (t < 64) {
@@ -144,7 +160,7 @@ __global__ __launch_bounds__(256, 2) void chunk_scan_kernel(
       s_R[ra][rb] = (rb <= ra) ? expf((float)(s_cs[ra * 32 + 31] - s_cs[rb * 32 + 31])) : 0.0f;
     }
   }
-  // ---- x^T [p][i] (fp16) and x rows [j][p] (fp16 input) in LDS
+  // ---- x^T [p][i] (fp16) in LDS
   {
     uint8_t* r0 = s_xT + p0 * kXTS + jb * 64;
     uint8_t* r1 = r0 + kXTS;
@@ -160,11 +176,6 @@ __global__ __launch_bounds__(256, 2) void chunk_scan_kernel(
       *reinterpret_cast<uint4*>(r0 + 16 * q) = make_uint4(a[0], a[1], a[2], a[3]);
       *reinterpret_cast<uint4*>(r1 + 16 * q) = make_uint4(bb[0], bb[1], bb[2], bb[3]);
     }
-    if constexpr (kHalfX) {
-#pragma unroll
-      for (int r = 0; r < 32; ++r)
-        *reinterpret_cast<uint32_t*>(s_xr + (jb * 32 + r) * kYS + p0 * 2) = (uint32_t)xr[r];
-    }
   }
   __syncthreads();
 
@@ -172,52 +183,42 @@ __global__ __launch_bounds__(256, 2) void chunk_scan_kernel(
   // lane owns one token row j and runs of 4 consecutive channels: the epilogue needs one row
   // factor per lane and moves 8-byte vectors.  Lane l: j = 32 jt + (l % 32); accumulator
   // register r holds channel p = 32 pt + 8 (r / 4) + 4 (l / 32) + r % 4.
-  const int8_t* pbase = pin + (((size_t)b * nc + c) * H + h) * (size_t)kP * kN;
-  const int8_t* cbbase = cbq + (((size_t)b * nc + c) * G + g) * (size_t)kQ * kQ;
+  // operand fragments (frag.hpp): 1 KB per fragment, this lane's 16 bytes at lane * 16
   const int pc = lane & 31, half = lane >> 5;
+  const size_t cg = ((size_t)b * nc + c) * G + g;
+  const int8_t* pbase = pin + (((size_t)b * nc + c) * H + h) * (size_t)kP * kN + lane * 16;
+  const int8_t* cbbase = cbq + cg * (size_t)frag::kCbChunkBytes + lane * 16;
+  const int8_t* cqbase = cq_frag + cg * (size_t)kQ * kN + lane * 16;
   const float Dh = Dv ? Dv[h] : 0.0f;
+  // packed fp16 output of the two j-blocks (8 runs of 4 channels each), staged after the loop
+  uint2 y_first[8], y_second[8];
 
-  for (int q2 = 0; q2 < 2; ++q2) {
-    const int jt = q2 ? 7 - wv : wv;
+  // One j-block of 32 tokens: Scan1, Scan2 and the epilogue; fp16 output packed into yo.
+  auto jblock = [&](const int jt, uint2 (&yo)[8]) {
+    // keeps the per-channel epilogue tables of the two calls from being loaded once and held
+    // across both (64 registers)
+    asm volatile("" ::: "memory");
     const int jrow = jt * 32 + pc;
-    // -- Scan1: Y1^T = P_in . C_q^T, int8 MFMA over n
-    v16i yi0 = {}, yi1 = {};
-    {
-      const int8_t* crow = Cq + ((tok0 + jrow) * G + g) * kN + 16 * half;
-      const int8_t* p0row = pbase + (size_t)pc * kN + 16 * half;
-      const int8_t* p1row = p0row + 32 * kN;
-      v4i a[4], b0[4], b1[4];
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        a[ks] = *reinterpret_cast<const v4i*>(crow + 32 * ks);
-        b0[ks] = *reinterpret_cast<const v4i*>(p0row + 32 * ks);
-        b1[ks] = *reinterpret_cast<const v4i*>(p1row + 32 * ks);
-      }
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        yi0 = __builtin_amdgcn_mfma_i32_32x32x32_i8(b0[ks], a[ks], yi0, 0, 0, 0);
-        yi1 = __builtin_amdgcn_mfma_i32_32x32x32_i8(b1[ks], a[ks], yi1, 0, 0, 0);
-      }
-    }
     // -- Scan2: y_diag^T = x^T . W^T, fp16 MFMA over the causal source tokens i; CB_q of
     //    block it+1 is prefetched while block it is built
     v16f yd0 = {}, yd1 = {};
     {
-      const int8_t* cbrow = cbbase + (size_t)jrow * kQ + 8 * half;
+      const int8_t* cbrow = cbbase + (size_t)frag::cb_block(jt, 0) * 1024;   // blocks (jt, it)
       const float csrj = s_csr[jrow];
-      uint2 cur0 = *reinterpret_cast<const uint2*>(cbrow);
-      uint2 cur1 = *reinterpret_cast<const uint2*>(cbrow + 16);
+      const float ej = __expf(csrj);                       // exp(cs_j - r_{J-1}), in (0, 1]
+      const bool diag_fast =
+          __builtin_amdgcn_readfirstlane((int)(s_csr[jt * 32 + 31] >= -kDiagSpan)) != 0;
+      uint4 cur = *reinterpret_cast<const uint4*>(cbrow);
       for (int it = 0; it <= jt; ++it) {
-        uint2 nx0 = cur0, nx1 = cur1;
+        uint4 nx = cur;
         if (it < jt) {
-          nx0 = *reinterpret_cast<const uint2*>(cbrow + (it + 1) * 32);
-          nx1 = *reinterpret_cast<const uint2*>(cbrow + (it + 1) * 32 + 16);
+          nx = *reinterpret_cast<const uint4*>(cbrow + (it + 1) * 1024);
         }
         // row factor of an off-diagonal block: exp(cs_j - r_{J-1}) exp(r_{J-1} - r_I)
-        const float vj = (it < jt) ? __expf(csrj) * s_R[jt - 1][it] : 0.0f;
+        const float vj = (it < jt) ? ej * s_R[jt - 1][it] : 0.0f;
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
-          const uint2 cb8 = ks ? cur1 : cur0;
+          const uint2 cb8 = ks ? make_uint2(cur.z, cur.w) : make_uint2(cur.x, cur.y);
           const int i0 = it * 32 + ks * 16 + 8 * half;
           // int8 weights as unsigned bytes (q + 128), 4 per dword
           const uint32_t ub0 = cb8.x ^ 0x80808080u, ub1 = cb8.y ^ 0x80808080u;
@@ -228,6 +229,16 @@ __global__ __launch_bounds__(256, 2) void chunk_scan_kernel(
               const float2 uu = s_u[i0 + e];
               const float qb = (float)(((e < 4 ? ub0 : ub1) >> (8 * (e & 3))) & 0xffu);
               wv[e] = __builtin_fmaf(qb, uu.x, uu.y) * vj;
+            }
+          } else if (diag_fast) {
+            // diagonal block of small span: exp(cs_j - cs_i) = exp(cs_j - r_{J-1}) exp(r_{J-1} - cs_i)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              const int i = i0 + e;
+              const float2 dd = s_ud[i];
+              const float qb = (float)(((e < 4 ? ub0 : ub1) >> (8 * (e & 3))) & 0xffu);
+              const float v = __builtin_fmaf(qb, dd.x, dd.y) * ej;
+              wv[e] = (i <= jrow) ? v : 0.0f;
             }
           } else {
             // diagonal block: exp per element; the clamp keeps the masked (i > j) entries finite
@@ -256,8 +267,30 @@ __global__ __launch_bounds__(256, 2) void chunk_scan_kernel(
           yd0 = __builtin_amdgcn_mfma_f32_32x32x16_f16(xa0, wf, yd0, 0, 0, 0);
           yd1 = __builtin_amdgcn_mfma_f32_32x32x16_f16(xa1, wf, yd1, 0, 0, 0);
         }
-        cur0 = nx0;
-        cur1 = nx1;
+        cur = nx;
+      }
+    }
+    // -- Scan1: Y1^T = P_in . C_q^T, int8 MFMA over n
+    v16i yi0 = {}, yi1 = {};
+    {
+      const int8_t* crow = cqbase + (size_t)jt * (kN / 32) * 1024;
+      // the P_in fragments are the same for both j-blocks; an opaque offset makes each call
+      // load them again (from L2) instead of holding 32 registers across the other block
+      int lofs = 0;
+      asm volatile("" : "+v"(lofs));
+      const int8_t* p0row = pbase + lofs;
+      const int8_t* p1row = p0row + (kN / 32) * 1024;
+      v4i a[4], b0[4], b1[4];
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        a[ks] = *reinterpret_cast<const v4i*>(crow + 1024 * ks);
+        b0[ks] = *reinterpret_cast<const v4i*>(p0row + 1024 * ks);
+        b1[ks] = *reinterpret_cast<const v4i*>(p1row + 1024 * ks);
+      }
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        yi0 = __builtin_amdgcn_mfma_i32_32x32x32_i8(b0[ks], a[ks], yi0, 0, 0, 0);
+        yi1 = __builtin_amdgcn_mfma_i32_32x32x32_i8(b1[ks], a[ks], yi1, 0, 0, 0);
       }
     }
     // -- epilogue of token row jrow: y = Y1 a_C exp(cs_j) a_S[p] + y_diag + D x + corr[p]
@@ -271,12 +304,10 @@ __global__ __launch_bounds__(256, 2) void chunk_scan_kernel(
         const float4 as4 = *reinterpret_cast<const float4*>(s_aS + pb);
         const float4 cr4 = *reinterpret_cast<const float4*>(s_cr + pb);
         float xv[4];
-        if constexpr (kHalfX) {
-          const uint2 xw = *reinterpret_cast<const uint2*>(s_xr + jrow * kYS + pb * 2);
-          xv[0] = (float)__builtin_bit_cast(_Float16, (uint16_t)(xw.x & 0xffffu));
-          xv[1] = (float)__builtin_bit_cast(_Float16, (uint16_t)(xw.x >> 16));
-          xv[2] = (float)__builtin_bit_cast(_Float16, (uint16_t)(xw.y & 0xffffu));
-          xv[3] = (float)__builtin_bit_cast(_Float16, (uint16_t)(xw.y >> 16));
+        if constexpr (sizeof(XT) == 2) {
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            xv[q] = (float)*reinterpret_cast<const _Float16*>(s_xT + (pb + q) * kXTS + jrow * 2);
         } else {
           const float4 xf = *reinterpret_cast<const float4*>(x + orow + pb);
           xv[0] = xf.x; xv[1] = xf.y; xv[2] = xf.z; xv[3] = xf.w;
@@ -290,7 +321,7 @@ __global__ __launch_bounds__(256, 2) void chunk_scan_kernel(
           const int r = 4 * g4 + q;
           yi[q] = pt ? yi1[r] : yi0[r];
           const float yd = pt ? yd1[r] : yd0[r];
-          v[q] = (((float)yi[q] * eo) * asv[q] + yd) + Dh * xv[q] + crv[q];
+          v[q] = __builtin_fmaf(Dh, xv[q], __builtin_fmaf((float)yi[q] * eo, asv[q], yd)) + crv[q];
         }
         if (y1_tap)
           *reinterpret_cast<int4*>(y1_tap + orow + pb) = make_int4(yi[0], yi[1], yi[2], yi[3]);
@@ -302,16 +333,33 @@ __global__ __launch_bounds__(256, 2) void chunk_scan_kernel(
                 ((uint32_t)__builtin_bit_cast(uint16_t, (_Float16)v[1]) << 16);
           o.y = (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)v[2]) |
                 ((uint32_t)__builtin_bit_cast(uint16_t, (_Float16)v[3]) << 16);
-          if constexpr (kHalfX)
-            *reinterpret_cast<uint2*>(s_xr + jrow * kYS + pb * 2) = o;   // in place over x
-          else
-            *reinterpret_cast<uint2*>(y + orow + pb) = o;
+          // pinned here: otherwise the arithmetic sinks to the stage writes after the other
+          // j-block and keeps this block's accumulators and tables alive across it
+          asm volatile("" : "+v"(o.x), "+v"(o.y));
+          yo[4 * pt + g4] = o;
         }
       }
     }
-  }
+  };
+  jblock(wv, y_first);
+  jblock(7 - wv, y_second);
 
-  if constexpr (sizeof(YT) == 2 && kHalfX) {
+  if constexpr (sizeof(YT) == 2) {
+    // fp16 output leaves through LDS as whole 128-byte token rows.  The stage reuses the x^T
+    // bytes once every wave is done with them: row j at 128 j, its 16-byte column chunk k at
+    // slot k ^ (j & 7) (conflict-free 8-byte writes by token and 16-byte reads by row).
+    __syncthreads();
+    uint8_t* s_y = s_xT;
+#pragma unroll
+    for (int q2 = 0; q2 < 2; ++q2) {
+      const int j = (q2 ? 7 - wv : wv) * 32 + pc;
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int slot = k ^ (j & 7);
+        *reinterpret_cast<uint2*>(s_y + j * 128 + slot * 16 + 8 * half) =
+            q2 ? y_second[k] : y_first[k];
+      }
+    }
     __syncthreads();
 #pragma unroll
     for (int k = 0; k < (kQ * kP * 2) / (16 * 256); ++k) {
@@ -319,7 +367,7 @@ __global__ __launch_bounds__(256, 2) void chunk_scan_kernel(
       const int j = idx >> 3, col = idx & 7;
       *reinterpret_cast<uint4*>(reinterpret_cast<uint8_t*>(y) +
                                 ((tok0 + j) * HP + (size_t)h * kP) * 2 + col * 16) =
-          *reinterpret_cast<const uint4*>(s_xr + j * kYS + col * 16);
+          *reinterpret_cast<const uint4*>(s_y + j * 128 + ((col ^ (j & 7)) * 16));
     }
   }
 }
@@ -327,7 +375,7 @@ __global__ __launch_bounds__(256, 2) void chunk_scan_kernel(
 }  // namespace
 
 hipError_t launch_chunk_scan(const LayerDims& d, const void* x, int x_dtype, const float* dt,
-                             int dt_softplus, const float* A, const int8_t* Cq,
+                             int dt_softplus, const float* A, const int8_t* cq_frag,
                              const float* C_scale, int c_per_token, const int8_t* pin,
                              const int8_t* cbq, const float* cb_scale, const float* state_scale,
                              const float* D, const float* corr, void* y, int y_dtype,
@@ -337,8 +385,9 @@ hipError_t launch_chunk_scan(const LayerDims& d, const void* x, int x_dtype, con
   const dim3 grid((unsigned)nwork), block(256);
 #define SSDI8_SCAN_LAUNCH(XT, YT)                                                             \
   hipLaunchKernelGGL((chunk_scan_kernel<XT, YT>), grid, block, 0, st,                         \
-                     static_cast<const XT*>(x), dt, A, Cq, C_scale, c_per_token, pin, cbq,    \
-                     cb_scale, state_scale, D, corr, dt_softplus, static_cast<YT*>(y), y1_tap, \
+                     static_cast<const XT*>(x), dt, A, cq_frag, C_scale, c_per_token, pin,    \
+                     cbq, cb_scale, state_scale, D, corr, dt_softplus, static_cast<YT*>(y),   \
+                     y1_tap,                                                                  \
                      d.seqlen, d.nheads, d.ngroups, d.nchunks)
   if (x_dtype == 1 && y_dtype == 1) SSDI8_SCAN_LAUNCH(_Float16, _Float16);
   else if (x_dtype == 1) SSDI8_SCAN_LAUNCH(_Float16, float);

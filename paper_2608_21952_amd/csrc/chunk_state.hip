@@ -12,8 +12,11 @@
 // The contraction runs over tokens, which are strided in HBM: x is loaded row-coalesced (32
 // lanes cover one 128-byte token row), quantized in registers and written to LDS already
 // transposed ([p][j], tokens contiguous = the MFMA K-slice); B_q^T comes pre-transposed from
-// the ChunkBMM kernel.  S_q leaves through an LDS stage as full 16-byte rows.
+// the ChunkBMM kernel in fragment order (frag.hpp).  S_q leaves through an LDS stage in the
+// fragment order in which ChunkScan1 reads the entering state (state passing is elementwise, so
+// it keeps that order); the optional S_q / S32 taps are row-major [p][n].
 #include "common.hpp"
+#include "frag.hpp"
 #include "launch.hpp"
 
 namespace ssdi8 {
@@ -52,7 +55,8 @@ __global__ __launch_bounds__(256) void chunk_state_kernel(
     const int8_t* __restrict__ bqT, const float* __restrict__ B_scale,
     const float* __restrict__ xs_scale, int xs_per_head, const float* __restrict__ state_scale,
     int dt_softplus, int shift, int8_t* __restrict__ sq, int16_t* __restrict__ qd,
-    int8_t* __restrict__ xq_tap, int32_t* __restrict__ s32_tap, int L, int H, int G, int nc) {
+    int8_t* __restrict__ xq_tap, int8_t* __restrict__ sq_tap, int32_t* __restrict__ s32_tap,
+    int L, int H, int G, int nc) {
   __shared__ __attribute__((aligned(16))) int8_t s_xq[kP * kXS];
   __shared__ float s_lut[kQ];
   __shared__ float s_inv[kP];
@@ -135,31 +139,36 @@ __global__ __launch_bounds__(256) void chunk_state_kernel(
   v16i acc0 = {}, acc1 = {};
   {
     const int8_t* arow = s_xq + (mt * 32 + (lane & 31)) * kXS;
-    const int8_t* b0row = bq + (size_t)(ntb * 32 + (lane & 31)) * kQ;
-    const int8_t* b1row = b0row + (size_t)32 * kQ;
+    // B_q^T fragments of n-tiles ntb, ntb + 1: 1 KB per (n-tile, 32-token block), lane-major
+    const int8_t* b0f = bq + (size_t)ntb * (kQ / 32) * 1024 + lane * 16;
+    const int8_t* b1f = b0f + (size_t)(kQ / 32) * 1024;
 #pragma unroll
     for (int ks = 0; ks < kQ / 32; ++ks) {
       const int kof = ks * 32 + 16 * (lane >> 5);
       const v4i a = *reinterpret_cast<const v4i*>(arow + kof);
-      const v4i b0 = *reinterpret_cast<const v4i*>(b0row + kof);
-      const v4i b1 = *reinterpret_cast<const v4i*>(b1row + kof);
+      const v4i b0 = *reinterpret_cast<const v4i*>(b0f + ks * 1024);
+      const v4i b1 = *reinterpret_cast<const v4i*>(b1f + ks * 1024);
       acc0 = __builtin_amdgcn_mfma_i32_32x32x32_i8(a, b0, acc0, 0, 0, 0);
       acc1 = __builtin_amdgcn_mfma_i32_32x32x32_i8(a, b1, acc1, 0, 0, 0);
     }
   }
   __syncthreads();  // X_q^T no longer read: its LDS is reused to stage S_q
 
-  // ---- requantize (Eq. 8) and stage S_q [p][n]
+  // ---- requantize (Eq. 8) and stage S_q in fragment order
   int8_t* s_stage = s_xq;
   const size_t sbase = (((size_t)b * nc + c) * H + h) * (size_t)kP * kN;
+  const int n0 = ntb * 32 + (lane & 31);
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
     const int p = mt * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-    const int n0 = ntb * 32 + (lane & 31);
     const float ms = s_ms[p];
-    s_stage[p * kN + n0] = (int8_t)requant_i8(acc0[r], ms);
-    s_stage[p * kN + n0 + 32] = (int8_t)requant_i8(acc1[r], ms);
-    if (s32_tap) {
+    s_stage[frag::kslice_offset(p, n0, kN)] = (int8_t)requant_i8(acc0[r], ms);
+    s_stage[frag::kslice_offset(p, n0 + 32, kN)] = (int8_t)requant_i8(acc1[r], ms);
+  }
+  if (s32_tap) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int p = mt * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
       s32_tap[sbase + (size_t)p * kN + n0] = acc0[r];
       s32_tap[sbase + (size_t)p * kN + n0 + 32] = acc1[r];
     }
@@ -169,6 +178,15 @@ __global__ __launch_bounds__(256) void chunk_state_kernel(
   const uint4* src = reinterpret_cast<const uint4*>(s_stage);
   dst[t] = src[t];
   dst[t + 256] = src[t + 256];
+  if (sq_tap) {
+    // row-major copy: 16 consecutive n of one p are one 16-byte slice of the stage
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      const int idx = k * 256 + t, p = idx >> 3, n = (idx & 7) * 16;
+      *reinterpret_cast<uint4*>(sq_tap + sbase + (size_t)p * kN + n) =
+          *reinterpret_cast<const uint4*>(s_stage + frag::kslice_offset(p, n, kN));
+    }
+  }
 }
 
 }  // namespace
@@ -177,19 +195,19 @@ hipError_t launch_chunk_state(const LayerDims& d, const void* x, int x_dtype, co
                               int dt_softplus, const float* A, const int8_t* bqT,
                               const float* B_scale, const float* xs_scale, int xs_per_head,
                               const float* state_scale, int shift, int8_t* sq, int16_t* qd,
-                              int8_t* xq_tap, int32_t* s32_tap, hipStream_t st) {
+                              int8_t* xq_tap, int8_t* sq_tap, int32_t* s32_tap, hipStream_t st) {
   const int64_t nwork = (int64_t)d.batch * d.nchunks * d.nheads;
   if (nwork == 0) return hipSuccess;
   if (x_dtype == 1) {
     hipLaunchKernelGGL(chunk_state_kernel<_Float16>, dim3((unsigned)nwork), dim3(256), 0, st,
                        static_cast<const _Float16*>(x), dt, A, bqT, B_scale, xs_scale,
-                       xs_per_head, state_scale, dt_softplus, shift, sq, qd, xq_tap, s32_tap,
-                       d.seqlen, d.nheads, d.ngroups, d.nchunks);
+                       xs_per_head, state_scale, dt_softplus, shift, sq, qd, xq_tap, sq_tap,
+                       s32_tap, d.seqlen, d.nheads, d.ngroups, d.nchunks);
   } else {
     hipLaunchKernelGGL(chunk_state_kernel<float>, dim3((unsigned)nwork), dim3(256), 0, st,
                        static_cast<const float*>(x), dt, A, bqT, B_scale, xs_scale, xs_per_head,
-                       state_scale, dt_softplus, shift, sq, qd, xq_tap, s32_tap, d.seqlen,
-                       d.nheads, d.ngroups, d.nchunks);
+                       state_scale, dt_softplus, shift, sq, qd, xq_tap, sq_tap, s32_tap,
+                       d.seqlen, d.nheads, d.ngroups, d.nchunks);
   }
   return hipGetLastError();
 }

@@ -1,0 +1,50 @@
+// MFMA fragment order of the int8 tensors that one kernel writes and a later one reads as MFMA
+// operands (workspace only; the public tensors and debug taps keep their row-major layouts).
+//
+// An int8 operand of v_mfma_i32_32x32x32_i8 is a 32-row tile with a 32-wide K block; lane l
+// holds row l % 32 and the 16 K values starting at 16 (l / 32).  Stored so that the 64 lanes'
+// 16-byte slices are consecutive, a wave fetches a whole fragment as one contiguous 1 KB run
+// instead of 32 partial rows.
+//   kslice order: tile (row / 32, k / 32) at ((row / 32) (K / 32) + k / 32) * 1 KB.
+//   CB order:     the 36 causal 32x32 blocks (J, I <= J) of a 256x256 chunk; lane l of block
+//                 (J, I) holds row j = 32 J + l % 32 and the bytes i = 32 I + 16 ks + 8 (l / 32)
+//                 + e (ks = 0, 1; e < 8) in the order [ks][e]: the two K-slices of the fp16
+//                 32x32x16 ChunkScan2 B operand.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace ssdi8 {
+namespace frag {
+
+constexpr int kCbBlocks = 36;
+constexpr int kCbChunkBytes = kCbBlocks * 1024;
+
+// Byte offset of element (row, k) of a rows x K int8 matrix (K % 32 == 0) in kslice order;
+// consecutive k with the same k / 16 are consecutive bytes.
+__host__ __device__ __forceinline__ size_t kslice_offset(int row, int k, int K) {
+  const int lane = (row & 31) + 32 * ((k & 31) >> 4);
+  return ((size_t)(row >> 5) * (K >> 5) + (k >> 5)) * 1024 + lane * 16 + (k & 15);
+}
+
+// Inverse of kslice_offset: the (row, k) of byte offset `off`.
+__host__ __device__ __forceinline__ void kslice_coords(size_t off, int K, int* row, int* k) {
+  const size_t blk = off >> 10;
+  const int kb = K >> 5;
+  const int lane = (int)((off >> 4) & 63);
+  *row = (int)(blk / kb) * 32 + (lane & 31);
+  *k = (int)(blk % kb) * 32 + 16 * (lane >> 5) + (int)(off & 15);
+}
+
+// Index of causal block (J, I), I <= J, within a chunk.
+__host__ __device__ __forceinline__ int cb_block(int J, int I) { return J * (J + 1) / 2 + I; }
+
+// Byte offset of in-block element (jj, ii) (0 <= jj, ii < 32) within its 1 KB CB block.
+__host__ __device__ __forceinline__ int cb_inblock(int jj, int ii) {
+  return (jj + 32 * ((ii >> 3) & 1)) * 16 + (ii >> 4) * 8 + (ii & 7);
+}
+
+}  // namespace frag
+}  // namespace ssdi8

@@ -18,11 +18,14 @@ hipError_t launch_quantize(const void* src, int src_dtype, int64_t b, int64_t l,
                            int64_t m, int gran, float* scale, int compute_scale, int8_t* dst,
                            hipStream_t st);
 
-// ChunkBMM (int8 C.B^T per chunk and group, causal, requantized) plus the per-chunk
-// transposed copy of B_q ([b, c, g, n, j]) that ChunkState reads as its MFMA operand.
+// ChunkBMM (int8 C.B^T per chunk and group, causal, requantized) plus the operand copies the
+// later kernels read, all in the fragment order of frag.hpp: CB_q (36 KB per chunk and group),
+// B_q^T of the chunk ([n][j] as kslice order, ChunkState) and C_q of the chunk ([j][n] as
+// kslice order, ChunkScan1).  The taps are row-major [j][i].
 hipError_t launch_chunk_bmm(const LayerDims& d, const int8_t* Cq, const int8_t* Bq,
                             const float* C_scale, int c_per_token, const float* B_scale,
-                            const float* cb_scale, int8_t* cbq, int32_t* cb32_tap, int8_t* bqT,
+                            const float* cb_scale, int8_t* cbq_frag, int8_t* cbq_tap,
+                            int32_t* cb32_tap, int8_t* bqT_frag, int8_t* cq_frag,
                             hipStream_t st);
 
 // ChunkCumsum + reformulated ChunkState (Eq. 7-8) and Q(Decay) (Eq. 9).
@@ -30,17 +33,20 @@ hipError_t launch_chunk_state(const LayerDims& d, const void* x, int x_dtype, co
                               int dt_softplus, const float* A, const int8_t* bqT,
                               const float* B_scale, const float* xs_scale, int xs_per_head,
                               const float* state_scale, int shift, int8_t* sq, int16_t* qd,
-                              int8_t* xq_tap, int32_t* s32_tap, hipStream_t st);
+                              int8_t* xq_tap, int8_t* sq_tap, int32_t* s32_tap, hipStream_t st);
 
 // INT8 StatePassing (Eq. 9) over [b, c, h, elems] slabs with elems = P*N (any P*N % 4 == 0).
+// frag_k = 0: S_q and P_in row-major; frag_k = N: both in kslice order with K = N (P, N
+// multiples of 32).  init, final_q, final_state and pin_tap are row-major either way.
 hipError_t launch_state_pass(int64_t batch, int64_t nchunks, int64_t nheads, int64_t elems,
                              int64_t headdim, const int8_t* sq, const int16_t* qd, int shift,
-                             int shift_round, const int8_t* init, int8_t* pin, int8_t* final_q,
-                             float* final_state, const float* state_scale, hipStream_t st);
+                             int shift_round, const int8_t* init, int8_t* pin, int8_t* pin_tap,
+                             int8_t* final_q, float* final_state, const float* state_scale,
+                             int frag_k, hipStream_t st);
 
-// ChunkScan1 (int8) + ChunkScan2 (fp16) + output epilogue.
+// ChunkScan1 (int8) + ChunkScan2 (fp16) + output epilogue; C_q, P_in and CB_q in fragment order.
 hipError_t launch_chunk_scan(const LayerDims& d, const void* x, int x_dtype, const float* dt,
-                             int dt_softplus, const float* A, const int8_t* Cq,
+                             int dt_softplus, const float* A, const int8_t* cq_frag,
                              const float* C_scale, int c_per_token, const int8_t* pin,
                              const int8_t* cbq, const float* cb_scale, const float* state_scale,
                              const float* D, const float* corr, void* y, int y_dtype,
