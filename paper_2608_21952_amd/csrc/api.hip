@@ -59,6 +59,9 @@ ssdi8_status check_dims(const ssdi8_dims* d) {
   if (xel > 4.0e12) return SSDI8_ERR_SHAPE;
   const double nwork = (double)d->batch * (d->seqlen / d->chunk) * d->nheads;
   if (nwork >= 2147483647.0) return SSDI8_ERR_SHAPE;
+  // the kernels address one chunk of one head's x / y rows with 32-bit byte offsets
+  if ((double)d->nheads * d->headdim * d->chunk * 4.0 >= 4294967296.0)
+    return SSDI8_ERR_UNSUPPORTED;
   return SSDI8_OK;
 }
 

@@ -59,19 +59,32 @@ __global__ __launch_bounds__(256) void chunk_bmm_kernel(
           *reinterpret_cast<const uint4*>(bbase + (size_t)j * rs + col);
     }
     __syncthreads();
-    const int n = t & 127, jh = t >> 7;
+    // two units of 4 channels n x 16 tokens j per thread: 16 dword reads (4 bytes of n per
+    // token row), four 4x4 byte transposes, then one 16-byte run of j per channel
     int8_t* dst = bqT_frag + cg * (size_t)kN * kQ;
 #pragma unroll
-    for (int blk = 0; blk < kQ / 32; ++blk) {
-      const int j0 = jh * (kQ / 2) + blk * 16;
-      uint32_t wd[4];
+    for (int u = 0; u < 2; ++u) {
+      const int n0 = 4 * (t & 31), j0 = 16 * ((t >> 5) + 8 * u);
+      uint32_t col[4][4];   // [n - n0][4-token group]
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        wd[u] = pack4_i8(s_b[(j0 + 4 * u) * kBS + n], s_b[(j0 + 4 * u + 1) * kBS + n],
-                         s_b[(j0 + 4 * u + 2) * kBS + n], s_b[(j0 + 4 * u + 3) * kBS + n]);
+      for (int g4 = 0; g4 < 4; ++g4) {
+        uint32_t r[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          r[i] = *reinterpret_cast<const uint32_t*>(s_b + (j0 + 4 * g4 + i) * kBS + n0);
+        const uint32_t a01 = __builtin_amdgcn_perm(r[1], r[0], 0x05010400u);
+        const uint32_t b01 = __builtin_amdgcn_perm(r[1], r[0], 0x07030602u);
+        const uint32_t a23 = __builtin_amdgcn_perm(r[3], r[2], 0x05010400u);
+        const uint32_t b23 = __builtin_amdgcn_perm(r[3], r[2], 0x07030602u);
+        col[0][g4] = __builtin_amdgcn_perm(a23, a01, 0x05040100u);
+        col[1][g4] = __builtin_amdgcn_perm(a23, a01, 0x07060302u);
+        col[2][g4] = __builtin_amdgcn_perm(b23, b01, 0x05040100u);
+        col[3][g4] = __builtin_amdgcn_perm(b23, b01, 0x07060302u);
       }
-      *reinterpret_cast<uint4*>(dst + frag::kslice_offset(n, j0, kQ)) =
-          make_uint4(wd[0], wd[1], wd[2], wd[3]);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        *reinterpret_cast<uint4*>(dst + frag::kslice_offset(n0 + i, j0, kQ)) =
+            make_uint4(col[i][0], col[i][1], col[i][2], col[i][3]);
     }
     return;
   }

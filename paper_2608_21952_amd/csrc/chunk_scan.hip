@@ -21,8 +21,8 @@
 // x is staged once in LDS as x^T [p][i] (fp16, tokens contiguous = the Scan2 MFMA K-slice); the
 // D skip term reads it back per token, and the fp16 output leaves through the same bytes as whole
 // 128-byte rows.  C_q, P_in and CB_q arrive in MFMA fragment order (frag.hpp), so every operand
-// load is one contiguous 1 KB run per wave.  About 45 KB of LDS and at most 168 VGPRs per lane
-// let three workgroups share a CU.
+// load is one contiguous 1 KB run per wave.  Under 40 KB of LDS and at most 128 VGPRs per lane
+// let four workgroups share a CU.
 #include "common.hpp"
 #include "frag.hpp"
 #include "launch.hpp"
@@ -41,16 +41,17 @@ constexpr float kDiagSpan = 64.0f;
 template <typename XT> struct Pair;
 template <> struct Pair<_Float16> {
   typedef uint32_t raw;
-  static __device__ __forceinline__ raw load(const _Float16* p) {
-    return *reinterpret_cast<const uint32_t*>(p);
+  static __device__ __forceinline__ raw load(__amdgpu_buffer_rsrc_t r, uint32_t vo, uint32_t so) {
+    return buf_load4(r, vo, so);
   }
   static __device__ __forceinline__ uint16_t lo(raw v) { return (uint16_t)(v & 0xffffu); }
   static __device__ __forceinline__ uint16_t hi(raw v) { return (uint16_t)(v >> 16); }
 };
 template <> struct Pair<float> {
   typedef float2 raw;
-  static __device__ __forceinline__ raw load(const float* p) {
-    return *reinterpret_cast<const float2*>(p);
+  static __device__ __forceinline__ raw load(__amdgpu_buffer_rsrc_t r, uint32_t vo, uint32_t so) {
+    const uint2 v = buf_load8(r, vo, so);
+    return make_float2(__uint_as_float(v.x), __uint_as_float(v.y));
   }
   static __device__ __forceinline__ uint16_t lo(raw v) {
     return __builtin_bit_cast(uint16_t, (_Float16)v.x);
@@ -71,7 +72,7 @@ __device__ __forceinline__ float softplus_fast(float v) {
 }
 
 template <typename XT, typename YT>
-__global__ __launch_bounds__(256, 3) void chunk_scan_kernel(
+__global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
     const XT* __restrict__ x, const float* __restrict__ dt, const float* __restrict__ A,
     const int8_t* __restrict__ cq_frag, const float* __restrict__ C_scale, int c_per_token,
     const int8_t* __restrict__ pin, const int8_t* __restrict__ cbq,
@@ -84,15 +85,14 @@ __global__ __launch_bounds__(256, 3) void chunk_scan_kernel(
     // Column tables of the ChunkScan2 weights, interleaved as (w, -128 w) pairs so that an int8
     // weight q, converted as the unsigned byte q + 128, gives fl32(q w) = fma(q + 128, w, -128 w)
     // exactly (the fma forms (q + 128) w - 128 w = q w before its one rounding).
-    float2 u[kQ];        // a_CB dt_i exp(r_I - cs_i)
-    float2 dtcb[kQ];     // a_CB dt_i
-    float2 ud[kQ];       // a_CB dt_i exp(r_{I-1} - cs_i), clamped (diagonal blocks of small span)
+    float2 u[kQ];        // a_CB dt_i exp(r_I - cs_i)                  (off-diagonal blocks)
+    float2 dg[kQ];       // a_CB dt_i exp(r_{I-1} - cs_i) if block I has a small span, else
+                         // a_CB dt_i                                   (diagonal blocks)
     float csr[kQ];       // cs_i - r_{I-1} (r_{-1} = 0), fp32
-    float eoff[kQ];      // a_C(j) exp(cs_j)
     float R[8][8];       // exp(r_a - r_b), b <= a
     float aS[kP];
     float cr[kP];
-    double cs[kQ];
+    double r[8];         // r_t: cs at the last token of block t
     double scan[4];
     // x^T [p][i] fp16: the ChunkScan2 MFMA operand and, for fp16 x, the D skip operand; then
     // the stage of the fp16 output (256 rows of 128 bytes).
@@ -100,14 +100,12 @@ __global__ __launch_bounds__(256, 3) void chunk_scan_kernel(
   };
   __shared__ Smem sm;
   float2* s_u = sm.u;
-  float2* s_dtcb = sm.dtcb;
-  float2* s_ud = sm.ud;
+  float2* s_dg = sm.dg;
   float* s_csr = sm.csr;
-  float* s_eoff = sm.eoff;
   float (*s_R)[8] = sm.R;
   float* s_aS = sm.aS;
   float* s_cr = sm.cr;
-  double* s_cs = sm.cs;
+  double* s_r = sm.r;
   double* s_scan = sm.scan;
   uint8_t* s_xT = sm.xT;
 
@@ -127,9 +125,10 @@ __global__ __launch_bounds__(256, 3) void chunk_scan_kernel(
   const int pp = t & 31, jb = t >> 5, p0 = 2 * pp;
   typename Pair<XT>::raw xr[32];
   {
-    const XT* xb = x + (tok0 + (size_t)jb * 32) * HP + (size_t)h * kP + p0;
+    const __amdgpu_buffer_rsrc_t xrs = buffer_rsrc(x + tok0 * HP + (size_t)h * kP);
+    const uint32_t xo = (uint32_t)((jb * 32 * HP + p0) * sizeof(XT));
 #pragma unroll
-    for (int r = 0; r < 32; ++r) xr[r] = Pair<XT>::load(xb + (size_t)r * HP);
+    for (int r = 0; r < 32; ++r) xr[r] = Pair<XT>::load(xrs, xo, (uint32_t)(r * HP * sizeof(XT)));
   }
 
   // ---- ChunkCumsum (fp64 sums; the factors derived from it only need fp32 accuracy here)
@@ -137,7 +136,7 @@ __global__ __launch_bounds__(256, 3) void chunk_scan_kernel(
   if (dt_softplus) dtv = softplus_fast(dtv);
   const float dA = dtv * A[h];
   const double cs = block_scan_f64_256((double)dA, s_scan);
-  s_cs[t] = cs;
+  if ((t & 31) == 31) s_r[t >> 5] = cs;
   if (t < kP) {
     s_aS[t] = state_scale[h * kP + t];
     s_cr[t] = corr ? corr[h * kP + t] : 0.0f;
@@ -145,19 +144,19 @@ __global__ __launch_bounds__(256, 3) void chunk_scan_kernel(
   __syncthreads();
   {
     const int blk = t >> 5;
+    const double rprev = blk ? s_r[blk - 1] : 0.0;
     const float dtcb = aCB * dtv;
-    const float u = dtcb * expf((float)(s_cs[blk * 32 + 31] - cs));
-    s_dtcb[t] = make_float2(dtcb, -128.0f * dtcb);
+    const float u = dtcb * expf((float)(s_r[blk] - cs));
     s_u[t] = make_float2(u, -128.0f * u);
-    const float csr = (float)(blk ? cs - s_cs[blk * 32 - 1] : cs);
+    const float csr = (float)(cs - rprev);
     s_csr[t] = csr;
-    const float ud = dtcb * expf(__builtin_fminf(-csr, 2.0f * kDiagSpan));
-    s_ud[t] = make_float2(ud, -128.0f * ud);
-    const float ac = c_per_token ? C_scale[(tok0 + t) * G + g] : C_scale[g];
-    s_eoff[t] = ac * expf((float)cs);
+    // the same test as the diagonal block's (on its last token's csr)
+    const bool small_span = (float)(s_r[blk] - rprev) >= -kDiagSpan;
+    const float dg = small_span ? dtcb * expf(__builtin_fminf(-csr, kDiagSpan)) : dtcb;
+    s_dg[t] = make_float2(dg, -128.0f * dg);
     if (t < 64) {
       const int ra = t >> 3, rb = t & 7;
-      s_R[ra][rb] = (rb <= ra) ? expf((float)(s_cs[ra * 32 + 31] - s_cs[rb * 32 + 31])) : 0.0f;
+      s_R[ra][rb] = (rb <= ra) ? expf((float)(s_r[ra] - s_r[rb])) : 0.0f;
     }
   }
   // ---- x^T [p][i] (fp16) in LDS
@@ -186,9 +185,11 @@ __global__ __launch_bounds__(256, 3) void chunk_scan_kernel(
   // operand fragments (frag.hpp): 1 KB per fragment, this lane's 16 bytes at lane * 16
   const int pc = lane & 31, half = lane >> 5;
   const size_t cg = ((size_t)b * nc + c) * G + g;
-  const int8_t* pbase = pin + (((size_t)b * nc + c) * H + h) * (size_t)kP * kN + lane * 16;
-  const int8_t* cbbase = cbq + cg * (size_t)frag::kCbChunkBytes + lane * 16;
-  const int8_t* cqbase = cq_frag + cg * (size_t)kQ * kN + lane * 16;
+  const uint32_t lane16 = lane * 16;
+  const __amdgpu_buffer_rsrc_t prs =
+      buffer_rsrc(pin + (((size_t)b * nc + c) * H + h) * (size_t)kP * kN);
+  const __amdgpu_buffer_rsrc_t cbrs = buffer_rsrc(cbq + cg * (size_t)frag::kCbChunkBytes);
+  const __amdgpu_buffer_rsrc_t cqrs = buffer_rsrc(cq_frag + cg * (size_t)kQ * kN);
   const float Dh = Dv ? Dv[h] : 0.0f;
   // packed fp16 output of the two j-blocks (8 runs of 4 channels each), staged after the loop
   uint2 y_first[8], y_second[8];
@@ -199,110 +200,18 @@ __global__ __launch_bounds__(256, 3) void chunk_scan_kernel(
     // across both (64 registers)
     asm volatile("" ::: "memory");
     const int jrow = jt * 32 + pc;
-    // -- Scan2: y_diag^T = x^T . W^T, fp16 MFMA over the causal source tokens i; CB_q of
-    //    block it+1 is prefetched while block it is built
-    v16f yd0 = {}, yd1 = {};
-    {
-      const int8_t* cbrow = cbbase + (size_t)frag::cb_block(jt, 0) * 1024;   // blocks (jt, it)
-      const float csrj = s_csr[jrow];
-      const float ej = __expf(csrj);                       // exp(cs_j - r_{J-1}), in (0, 1]
-      const bool diag_fast =
-          __builtin_amdgcn_readfirstlane((int)(s_csr[jt * 32 + 31] >= -kDiagSpan)) != 0;
-      uint4 cur = *reinterpret_cast<const uint4*>(cbrow);
-      for (int it = 0; it <= jt; ++it) {
-        uint4 nx = cur;
-        if (it < jt) {
-          nx = *reinterpret_cast<const uint4*>(cbrow + (it + 1) * 1024);
-        }
-        // row factor of an off-diagonal block: exp(cs_j - r_{J-1}) exp(r_{J-1} - r_I)
-        const float vj = (it < jt) ? ej * s_R[jt - 1][it] : 0.0f;
-#pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-          const uint2 cb8 = ks ? make_uint2(cur.z, cur.w) : make_uint2(cur.x, cur.y);
-          const int i0 = it * 32 + ks * 16 + 8 * half;
-          // int8 weights as unsigned bytes (q + 128), 4 per dword
-          const uint32_t ub0 = cb8.x ^ 0x80808080u, ub1 = cb8.y ^ 0x80808080u;
-          float wv[8];
-          if (it < jt) {
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-              const float2 uu = s_u[i0 + e];
-              const float qb = (float)(((e < 4 ? ub0 : ub1) >> (8 * (e & 3))) & 0xffu);
-              wv[e] = __builtin_fmaf(qb, uu.x, uu.y) * vj;
-            }
-          } else if (diag_fast) {
-            // diagonal block of small span: exp(cs_j - cs_i) = exp(cs_j - r_{J-1}) exp(r_{J-1} - cs_i)
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-              const int i = i0 + e;
-              const float2 dd = s_ud[i];
-              const float qb = (float)(((e < 4 ? ub0 : ub1) >> (8 * (e & 3))) & 0xffu);
-              const float v = __builtin_fmaf(qb, dd.x, dd.y) * ej;
-              wv[e] = (i <= jrow) ? v : 0.0f;
-            }
-          } else {
-            // diagonal block: exp per element; the clamp keeps the masked (i > j) entries finite
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-              const int i = i0 + e;
-              const float2 dd = s_dtcb[i];
-              const float qb = (float)(((e < 4 ? ub0 : ub1) >> (8 * (e & 3))) & 0xffu);
-              const float ex = __expf(__builtin_fminf(csrj - s_csr[i], 0.0f));
-              const float v = __builtin_fmaf(qb, dd.x, dd.y) * ex;
-              wv[e] = (i <= jrow) ? v : 0.0f;
-            }
-          }
-          v8h wf;
-#pragma unroll
-          for (int e = 0; e < 8; e += 2) {
-            typedef float f2_t __attribute__((ext_vector_type(2)));
-            typedef _Float16 h2_t __attribute__((ext_vector_type(2)));
-            const f2_t pr = {wv[e], wv[e + 1]};
-            const h2_t hh = __builtin_convertvector(pr, h2_t);
-            wf[e] = hh.x;
-            wf[e + 1] = hh.y;
-          }
-          const v8h xa0 = *reinterpret_cast<const v8h*>(s_xT + pc * kXTS + i0 * 2);
-          const v8h xa1 = *reinterpret_cast<const v8h*>(s_xT + (32 + pc) * kXTS + i0 * 2);
-          yd0 = __builtin_amdgcn_mfma_f32_32x32x16_f16(xa0, wf, yd0, 0, 0, 0);
-          yd1 = __builtin_amdgcn_mfma_f32_32x32x16_f16(xa1, wf, yd1, 0, 0, 0);
-        }
-        cur = nx;
-      }
-    }
-    // -- Scan1: Y1^T = P_in . C_q^T, int8 MFMA over n
-    v16i yi0 = {}, yi1 = {};
-    {
-      const int8_t* crow = cqbase + (size_t)jt * (kN / 32) * 1024;
-      // the P_in fragments are the same for both j-blocks; an opaque offset makes each call
-      // load them again (from L2) instead of holding 32 registers across the other block
-      int lofs = 0;
-      asm volatile("" : "+v"(lofs));
-      const int8_t* p0row = pbase + lofs;
-      const int8_t* p1row = p0row + (kN / 32) * 1024;
-      v4i a[4], b0[4], b1[4];
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        a[ks] = *reinterpret_cast<const v4i*>(crow + 1024 * ks);
-        b0[ks] = *reinterpret_cast<const v4i*>(p0row + 1024 * ks);
-        b1[ks] = *reinterpret_cast<const v4i*>(p1row + 1024 * ks);
-      }
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        yi0 = __builtin_amdgcn_mfma_i32_32x32x32_i8(b0[ks], a[ks], yi0, 0, 0, 0);
-        yi1 = __builtin_amdgcn_mfma_i32_32x32x32_i8(b1[ks], a[ks], yi1, 0, 0, 0);
-      }
-    }
-    // -- epilogue of token row jrow: y = Y1 a_C exp(cs_j) a_S[p] + y_diag + D x + corr[p]
-    const float eo = s_eoff[jrow];
+    const float csrj = s_csr[jrow];
+    const float ej = __expf(csrj);                         // exp(cs_j - r_{J-1}), in (0, 1]
     const size_t orow = (tok0 + jrow) * HP + (size_t)h * kP;
+    // -- the Scan2 accumulators start from D x + corr[p] (the skip and correction terms)
+    v16f yd0, yd1;
 #pragma unroll
     for (int pt = 0; pt < 2; ++pt) {
 #pragma unroll
       for (int g4 = 0; g4 < 4; ++g4) {
         const int pb = pt * 32 + 8 * g4 + 4 * half;
-        const float4 as4 = *reinterpret_cast<const float4*>(s_aS + pb);
         const float4 cr4 = *reinterpret_cast<const float4*>(s_cr + pb);
+        const float crv[4] = {cr4.x, cr4.y, cr4.z, cr4.w};
         float xv[4];
         if constexpr (sizeof(XT) == 2) {
 #pragma unroll
@@ -312,8 +221,124 @@ __global__ __launch_bounds__(256, 3) void chunk_scan_kernel(
           const float4 xf = *reinterpret_cast<const float4*>(x + orow + pb);
           xv[0] = xf.x; xv[1] = xf.y; xv[2] = xf.z; xv[3] = xf.w;
         }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const float v0 = __builtin_fmaf(Dh, xv[q], crv[q]);
+          if (pt) yd1[4 * g4 + q] = v0;
+          else yd0[4 * g4 + q] = v0;
+        }
+      }
+    }
+    // -- Scan2: y_diag^T = x^T . W^T, fp16 MFMA over the causal source tokens i; CB_q of
+    //    block it+1 is prefetched while block it is built
+    {
+      const uint32_t cbrow = frag::cb_block(jt, 0) * 1024;   // blocks (jt, it)
+      const bool diag_fast =
+          __builtin_amdgcn_readfirstlane((int)(s_csr[jt * 32 + 31] >= -kDiagSpan)) != 0;
+      // W^T fragment of a 32x32 block (8 weights of this lane's token row per K-slice, as fp16)
+      // times the x^T fragments of both channel tiles
+      auto mfma_block = [&](const float (&wv)[8], int i0) {
+        v8h wf;
+#pragma unroll
+        for (int e = 0; e < 8; e += 2) {
+          typedef float f2_t __attribute__((ext_vector_type(2)));
+          typedef _Float16 h2_t __attribute__((ext_vector_type(2)));
+          const h2_t hh = __builtin_convertvector((f2_t){wv[e], wv[e + 1]}, h2_t);
+          wf[e] = hh.x;
+          wf[e + 1] = hh.y;
+        }
+        const v8h xa0 = *reinterpret_cast<const v8h*>(s_xT + pc * kXTS + i0 * 2);
+        const v8h xa1 = *reinterpret_cast<const v8h*>(s_xT + (32 + pc) * kXTS + i0 * 2);
+        yd0 = __builtin_amdgcn_mfma_f32_32x32x16_f16(xa0, wf, yd0, 0, 0, 0);
+        yd1 = __builtin_amdgcn_mfma_f32_32x32x16_f16(xa1, wf, yd1, 0, 0, 0);
+      };
+      // int8 weight e of a K-slice as the unsigned byte q + 128
+      auto qbyte = [](uint32_t ub0, uint32_t ub1, int e) {
+        return (float)(((e < 4 ? ub0 : ub1) >> (8 * (e & 3))) & 0xffu);
+      };
+      uint4 cur = buf_load16(cbrs, lane16, cbrow);
+      // off-diagonal blocks it < jt: straight-line body, CB_q of block it+1 (the diagonal block
+      // after the last one) in flight meanwhile
+      for (int it = 0; it < jt; ++it) {
+        const uint4 nx = buf_load16(cbrs, lane16, cbrow + (it + 1) * 1024);
+        // row factor: exp(cs_j - r_{J-1}) exp(r_{J-1} - r_I)
+        const float vj = ej * s_R[jt - 1][it];
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+          const int i0 = it * 32 + ks * 16 + 8 * half;
+          const uint32_t ub0 = (ks ? cur.z : cur.x) ^ 0x80808080u;
+          const uint32_t ub1 = (ks ? cur.w : cur.y) ^ 0x80808080u;
+          float wv[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const float2 uu = s_u[i0 + e];
+            wv[e] = __builtin_fmaf(qbyte(ub0, ub1, e), uu.x, uu.y) * vj;
+          }
+          mfma_block(wv, i0);
+        }
+        cur = nx;
+      }
+      // diagonal block it = jt, masked to i <= j
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) {
+        const int i0 = jt * 32 + ks * 16 + 8 * half;
+        const uint32_t ub0 = (ks ? cur.z : cur.x) ^ 0x80808080u;
+        const uint32_t ub1 = (ks ? cur.w : cur.y) ^ 0x80808080u;
+        float wv[8];
+        if (diag_fast) {
+          // small span: exp(cs_j - cs_i) = exp(cs_j - r_{J-1}) exp(r_{J-1} - cs_i)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const float2 dd = s_dg[i0 + e];
+            const float v = __builtin_fmaf(qbyte(ub0, ub1, e), dd.x, dd.y) * ej;
+            wv[e] = (i0 + e <= jrow) ? v : 0.0f;
+          }
+        } else {
+          // exp per element; the clamp keeps the masked (i > j) entries finite
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const float2 dd = s_dg[i0 + e];
+            const float ex = __expf(__builtin_fminf(csrj - s_csr[i0 + e], 0.0f));
+            const float v = __builtin_fmaf(qbyte(ub0, ub1, e), dd.x, dd.y) * ex;
+            wv[e] = (i0 + e <= jrow) ? v : 0.0f;
+          }
+        }
+        mfma_block(wv, i0);
+      }
+    }
+    // -- Scan1: Y1^T = P_in . C_q^T, int8 MFMA over n
+    v16i yi0 = {}, yi1 = {};
+    {
+      const uint32_t crow = jt * (kN / 32) * 1024;
+      // the P_in fragments are the same for both j-blocks; an opaque offset makes each call
+      // load them again (from L2) instead of holding 32 registers across the other block
+      uint32_t lofs = lane16;
+      asm volatile("" : "+v"(lofs));
+      constexpr uint32_t p1row = (kN / 32) * 1024;
+      v4i a[4], b0[4], b1[4];
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        a[ks] = __builtin_bit_cast(v4i, buf_load16(cqrs, lane16, crow + 1024 * ks));
+        b0[ks] = __builtin_bit_cast(v4i, buf_load16(prs, lofs, 1024 * ks));
+        b1[ks] = __builtin_bit_cast(v4i, buf_load16(prs, lofs, p1row + 1024 * ks));
+      }
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        yi0 = __builtin_amdgcn_mfma_i32_32x32x32_i8(b0[ks], a[ks], yi0, 0, 0, 0);
+        yi1 = __builtin_amdgcn_mfma_i32_32x32x32_i8(b1[ks], a[ks], yi1, 0, 0, 0);
+      }
+    }
+    // -- epilogue of token row jrow: y = Y1 a_C exp(cs_j) a_S[p] + (y_diag + D x + corr[p])
+    // a_C(j) exp(cs_j) = a_C(j) exp(cs_j - r_{J-1}) exp(r_{J-1})
+    const float ac = c_per_token ? C_scale[(tok0 + jrow) * G + g] : C_scale[g];
+    const float eo = ac * ej * (jt ? __expf((float)s_r[jt - 1]) : 1.0f);
+#pragma unroll
+    for (int pt = 0; pt < 2; ++pt) {
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4) {
+        const int pb = pt * 32 + 8 * g4 + 4 * half;
+        const float4 as4 = *reinterpret_cast<const float4*>(s_aS + pb);
         const float asv[4] = {as4.x, as4.y, as4.z, as4.w};
-        const float crv[4] = {cr4.x, cr4.y, cr4.z, cr4.w};
         float v[4];
         int yi[4];
 #pragma unroll
@@ -321,18 +346,18 @@ __global__ __launch_bounds__(256, 3) void chunk_scan_kernel(
           const int r = 4 * g4 + q;
           yi[q] = pt ? yi1[r] : yi0[r];
           const float yd = pt ? yd1[r] : yd0[r];
-          v[q] = __builtin_fmaf(Dh, xv[q], __builtin_fmaf((float)yi[q] * eo, asv[q], yd)) + crv[q];
+          v[q] = __builtin_fmaf((float)yi[q] * eo, asv[q], yd);
         }
         if (y1_tap)
           *reinterpret_cast<int4*>(y1_tap + orow + pb) = make_int4(yi[0], yi[1], yi[2], yi[3]);
         if constexpr (sizeof(YT) == 4) {
           *reinterpret_cast<float4*>(y + orow + pb) = make_float4(v[0], v[1], v[2], v[3]);
         } else {
-          uint2 o;
-          o.x = (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)v[0]) |
-                ((uint32_t)__builtin_bit_cast(uint16_t, (_Float16)v[1]) << 16);
-          o.y = (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)v[2]) |
-                ((uint32_t)__builtin_bit_cast(uint16_t, (_Float16)v[3]) << 16);
+          typedef float f2_t __attribute__((ext_vector_type(2)));
+          typedef _Float16 h2_t __attribute__((ext_vector_type(2)));
+          const h2_t h01 = __builtin_convertvector((f2_t){v[0], v[1]}, h2_t);
+          const h2_t h23 = __builtin_convertvector((f2_t){v[2], v[3]}, h2_t);
+          uint2 o = make_uint2(__builtin_bit_cast(uint32_t, h01), __builtin_bit_cast(uint32_t, h23));
           // pinned here: otherwise the arithmetic sinks to the stage writes after the other
           // j-block and keeps this block's accumulators and tables alive across it
           asm volatile("" : "+v"(o.x), "+v"(o.y));
@@ -350,24 +375,30 @@ __global__ __launch_bounds__(256, 3) void chunk_scan_kernel(
     // slot k ^ (j & 7) (conflict-free 8-byte writes by token and 16-byte reads by row).
     __syncthreads();
     uint8_t* s_y = s_xT;
-#pragma unroll
-    for (int q2 = 0; q2 < 2; ++q2) {
-      const int j = (q2 ? 7 - wv : wv) * 32 + pc;
+    {
+      // this lane's rows are 32 jt + pc, so j & 7 = pc & 7 for both j-blocks
+      const uint32_t jx = pc & 7;
+      uint8_t* r0 = s_y + (wv * 32 + pc) * 128 + 8 * half;
+      uint8_t* r1 = s_y + ((7 - wv) * 32 + pc) * 128 + 8 * half;
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
-        const int slot = k ^ (j & 7);
-        *reinterpret_cast<uint2*>(s_y + j * 128 + slot * 16 + 8 * half) =
-            q2 ? y_second[k] : y_first[k];
+        const uint32_t so = (k ^ jx) * 16;
+        *reinterpret_cast<uint2*>(r0 + so) = y_first[k];
+        *reinterpret_cast<uint2*>(r1 + so) = y_second[k];
       }
     }
     __syncthreads();
+    {
+      // thread: token rows 32 k + t / 8 (k = 0..7), 16-byte column t % 8; (t / 8) & 7 is the
+      // row's swizzle for every k
+      const int jt8 = t >> 3, col = t & 7;
+      const uint8_t* src = s_y + jt8 * 128 + ((col ^ (jt8 & 7)) * 16);
+      const __amdgpu_buffer_rsrc_t yrs = buffer_rsrc(y + tok0 * HP + (size_t)h * kP);
+      const uint32_t yo = (uint32_t)(jt8 * HP * 2 + col * 16);
 #pragma unroll
-    for (int k = 0; k < (kQ * kP * 2) / (16 * 256); ++k) {
-      const int idx = k * 256 + t;
-      const int j = idx >> 3, col = idx & 7;
-      *reinterpret_cast<uint4*>(reinterpret_cast<uint8_t*>(y) +
-                                ((tok0 + j) * HP + (size_t)h * kP) * 2 + col * 16) =
-          *reinterpret_cast<const uint4*>(s_y + j * 128 + ((col ^ (j & 7)) * 16));
+      for (int k = 0; k < (kQ * kP * 2) / (16 * 256); ++k)
+        buf_store16(*reinterpret_cast<const uint4*>(src + k * 32 * 128), yrs, yo,
+                    (uint32_t)(k * 32 * HP * 2));
     }
   }
 }

@@ -17,6 +17,35 @@ typedef int v16i __attribute__((ext_vector_type(16)));
 typedef float v16f __attribute__((ext_vector_type(16)));
 typedef _Float16 v8h __attribute__((ext_vector_type(8)));
 
+// Raw buffer resource over the bytes from `base` (gfx9 layout: 48-bit base, stride 0, no range
+// limit, dword 3 = 0x00020000).  A buffer access adds a per-lane 32-bit offset and a wave-uniform
+// 32-bit offset on the address unit, where a global access needs a 64-bit vector add per
+// access.  Callers keep every offset inside the tensor they address.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)0xffffffffu,
+                                           0x00020000);
+}
+__device__ __forceinline__ uint4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t voff,
+                                            uint32_t soff) {
+  const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, (int)soff, 0);
+  return make_uint4(v[0], v[1], v[2], v[3]);
+}
+__device__ __forceinline__ uint2 buf_load8(__amdgpu_buffer_rsrc_t r, uint32_t voff,
+                                           uint32_t soff) {
+  const auto v = __builtin_amdgcn_raw_buffer_load_b64(r, (int)voff, (int)soff, 0);
+  return make_uint2(v[0], v[1]);
+}
+__device__ __forceinline__ uint32_t buf_load4(__amdgpu_buffer_rsrc_t r, uint32_t voff,
+                                              uint32_t soff) {
+  return __builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, (int)soff, 0);
+}
+__device__ __forceinline__ void buf_store16(uint4 d, __amdgpu_buffer_rsrc_t r, uint32_t voff,
+                                            uint32_t soff) {
+  typedef uint32_t u32x4 __attribute__((vector_size(16)));
+  const u32x4 v = {d.x, d.y, d.z, d.w};
+  __builtin_amdgcn_raw_buffer_store_b128(v, r, (int)voff, (int)soff, 0);
+}
+
 // Symmetric int8 quantization of an fp32 value with a precomputed inverse step:
 // clamp(rne(v * inv), -127, 127).  One IEEE fp32 product, round-half-even to integer.
 __device__ __forceinline__ int quant_i8(float v, float inv) {

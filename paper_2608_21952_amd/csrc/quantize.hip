@@ -24,15 +24,15 @@ __device__ __forceinline__ int64_t granule_of(int64_t e, int gran, int64_t k, in
 }
 
 // 16 consecutive elements per thread; requires m % 16 == 0 (all 16 share one (b,l,k) row).
-template <typename T>
+// I is the index type: 32-bit whenever the element count allows (no 64-bit divisions).
+template <typename T, typename I>
 __global__ __launch_bounds__(256) void quant_static_vec16(const T* __restrict__ src,
                                                           int8_t* __restrict__ dst,
                                                           const float* __restrict__ scale,
-                                                          int gran, int64_t nvec, int64_t k,
-                                                          int64_t m) {
-  for (int64_t v = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; v < nvec;
-       v += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t e0 = v * 16;
+                                                          int gran, I nvec, I k, I m) {
+  const I rowvecs = m / 16;
+  for (I v = (I)blockIdx.x * blockDim.x + threadIdx.x; v < nvec; v += (I)gridDim.x * blockDim.x) {
+    const I e0 = v * 16;
     float x[16];
     if constexpr (sizeof(T) == 2) {
       const uint4* s = reinterpret_cast<const uint4*>(src + e0);
@@ -52,12 +52,15 @@ __global__ __launch_bounds__(256) void quant_static_vec16(const T* __restrict__ 
         x[4 * i] = f.x; x[4 * i + 1] = f.y; x[4 * i + 2] = f.z; x[4 * i + 3] = f.w;
       }
     }
+    const I row = v / rowvecs;
     int q[16];
     if (gran == 2) {
+      const I c0 = (row % k) * m + (v - row * rowvecs) * 16;   // channel of element 0
 #pragma unroll
-      for (int i = 0; i < 16; ++i) q[i] = quant_i8(x[i], 1.0f / scale[(e0 + i) % (k * m)]);
+      for (int i = 0; i < 16; ++i) q[i] = quant_i8(x[i], 1.0f / scale[c0 + i]);
     } else {
-      const float inv = 1.0f / scale[granule_of(e0, gran, k, m)];
+      const I gi = gran == 0 ? 0 : (gran == 1 ? row % k : row);
+      const float inv = 1.0f / scale[gi];
 #pragma unroll
       for (int i = 0; i < 16; ++i) q[i] = quant_i8(x[i], inv);
     }
@@ -170,8 +173,15 @@ hipError_t quantize_impl(const T* src, int64_t b, int64_t l, int64_t k, int64_t 
   if (n == 0) return hipGetLastError();
   if (m % 16 == 0) {
     const int64_t nvec = n / 16;
-    hipLaunchKernelGGL(quant_static_vec16<T>, dim3((unsigned)grid_for(nvec)), dim3(256), 0, st,
-                       src, dst, scale, gran, nvec, k, m);
+    if (n < ((int64_t)1 << 31)) {
+      hipLaunchKernelGGL((quant_static_vec16<T, uint32_t>), dim3((unsigned)grid_for(nvec)),
+                         dim3(256), 0, st, src, dst, scale, gran, (uint32_t)nvec, (uint32_t)k,
+                         (uint32_t)m);
+    } else {
+      hipLaunchKernelGGL((quant_static_vec16<T, uint64_t>), dim3((unsigned)grid_for(nvec)),
+                         dim3(256), 0, st, src, dst, scale, gran, (uint64_t)nvec, (uint64_t)k,
+                         (uint64_t)m);
+    }
   } else {
     hipLaunchKernelGGL(quant_static_scalar<T>, dim3((unsigned)grid_for(n)), dim3(256), 0, st,
                        src, dst, scale, gran, n, k, m);
