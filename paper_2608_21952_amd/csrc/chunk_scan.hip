@@ -229,6 +229,7 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
         }
       }
     }
+    v4i a[4], b0[4], b1[4];   // ChunkScan1 operands
     // -- Scan2: y_diag^T = x^T . W^T, fp16 MFMA over the causal source tokens i; CB_q of
     //    block it+1 is prefetched while block it is built
     {
@@ -261,6 +262,9 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
       // after the last one) in flight meanwhile
       for (int it = 0; it < jt; ++it) {
         const uint4 nx = buf_load16(cbrs, lane16, cbrow + (it + 1) * 1024);
+        // keep the prefetch at the top of the body (left alone, the scheduler sinks it to the
+        // end, and the next iteration waits for the full L2 latency)
+        __builtin_amdgcn_sched_barrier(0);
         // row factor: exp(cs_j - r_{J-1}) exp(r_{J-1} - r_I)
         const float vj = ej * s_R[jt - 1][it];
 #pragma unroll
@@ -277,6 +281,14 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
           mfma_block(wv, i0);
         }
         cur = nx;
+      }
+      // the C_q fragments of ChunkScan1, in flight during the diagonal block
+      {
+        const uint32_t crow = jt * (kN / 32) * 1024;
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks)
+          a[ks] = __builtin_bit_cast(v4i, buf_load16(cqrs, lane16, crow + 1024 * ks));
+        __builtin_amdgcn_sched_barrier(0);
       }
       // diagonal block it = jt, masked to i <= j
 #pragma unroll
@@ -309,16 +321,13 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
     // -- Scan1: Y1^T = P_in . C_q^T, int8 MFMA over n
     v16i yi0 = {}, yi1 = {};
     {
-      const uint32_t crow = jt * (kN / 32) * 1024;
       // the P_in fragments are the same for both j-blocks; an opaque offset makes each call
       // load them again (from L2) instead of holding 32 registers across the other block
       uint32_t lofs = lane16;
       asm volatile("" : "+v"(lofs));
       constexpr uint32_t p1row = (kN / 32) * 1024;
-      v4i a[4], b0[4], b1[4];
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) {
-        a[ks] = __builtin_bit_cast(v4i, buf_load16(cqrs, lane16, crow + 1024 * ks));
         b0[ks] = __builtin_bit_cast(v4i, buf_load16(prs, lofs, 1024 * ks));
         b1[ks] = __builtin_bit_cast(v4i, buf_load16(prs, lofs, p1row + 1024 * ks));
       }
