@@ -68,16 +68,17 @@ def measured_traffic(kernel: str, workload: str):
 
 
 def cpu_baseline(cfg, inp, sc, budget_s: float):
-    """The CPU oracle as it stands, timed on a bounded sample: batch element 0, the first
-    `nh` heads (all chunks), nh sized from a one-head pilot to about `budget_s` seconds."""
+    """The CPU oracle as it stands, timed on a bounded sample of the workload: the first `nh`
+    heads of the first `nb` batch elements (all chunks), sized from pilots to about `budget_s`
+    seconds; the whole workload when it fits."""
     import numpy as np
     import threadpoolctl
     from oracle import int8
 
-    def run(nh):
+    def run(nb, nh):
         t = time.perf_counter()
-        int8.ssdi8_forward(inp["x"][:1, :, :nh], inp["dt_raw"][:1, :, :nh], inp["A"][:nh],
-                           inp["B"][:1], inp["C"][:1], inp["D"][:nh], sc["corr"][:nh],
+        int8.ssdi8_forward(inp["x"][:nb, :, :nh], inp["dt_raw"][:nb, :, :nh], inp["A"][:nh],
+                           inp["B"][:nb], inp["C"][:nb], inp["D"][:nh], sc["corr"][:nh],
                            {"alpha_B": sc["alpha_B"], "alpha_C": sc["alpha_C"],
                             "alpha_Xs": sc["alpha_Xs"][:nh], "alpha_S": sc["alpha_S"][:nh],
                             "alpha_CB": sc["alpha_CB"]},
@@ -86,18 +87,24 @@ def cpu_baseline(cfg, inp, sc, budget_s: float):
 
     G = cfg.ngroups
     hpg = cfg.nheads // G
-    pilot = run(1)
+    pilot = run(1, 1)
     nh = int(max(1, min(cfg.nheads, budget_s / max(pilot, 1e-3))))
-    if G > 1:
-        nh = min(nh, hpg)                     # stay inside group 0 (its B, C were sliced)
-    t = run(nh)
+    nb = 1
+    if nh < cfg.nheads and G > 1:
+        nh = min(nh, hpg)                     # stay inside group 0
+    if nh == cfg.nheads:
+        one = run(1, nh)
+        nb = int(max(1, min(cfg.batch, budget_s / max(one, 1e-3))))
+    t = run(nb, nh)
     info = threadpoolctl.threadpool_info()
     threads = max([i.get("num_threads", 1) for i in info] or [1])
-    tokens = cfg.seqlen * nh / cfg.nheads     # layer-tokens: a token carries all H heads
+    tokens = nb * cfg.seqlen * nh / cfg.nheads   # layer-tokens: a token carries all H heads
+    whole = nb == cfg.batch and nh == cfg.nheads
+    what = ("the whole workload" if whole else
+            f"batch elements 0..{nb - 1} of {cfg.batch}, heads 0..{nh - 1} of {cfg.nheads}")
     return {"value": tokens / t, "unit": "tokens/s", "cores": threads, "kind": "oracle",
-            "sample": f"batch element 0, heads 0..{nh - 1} of {cfg.nheads}, {cfg.seqlen} "
-                      f"tokens ({t:.1f} s; tokens/s counted as layer tokens = "
-                      f"token-heads / {cfg.nheads})",
+            "sample": f"{what}, {cfg.seqlen} tokens each ({t:.1f} s; tokens/s counted as layer "
+                      f"tokens = token-heads / {cfg.nheads})",
             "seconds": round(t, 2), "host_cpus": len(os.sched_getaffinity(0))}
 
 
