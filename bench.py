@@ -21,6 +21,8 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0           # MI355X HBM3E, published
+INT8_PEAK_TOPS = 5000.0         # MI355X dense int8 MFMA, published
+FP16_PEAK_TFLOPS = 2500.0       # MI355X dense fp16 MFMA, published
 MODULES = ("chunk_bmm", "chunk_state", "state_pass", "chunk_scan")
 
 
@@ -39,6 +41,20 @@ def algorithmic_bytes(cfg):
         "chunk_state": T * H * P * sx + T * H * 4 + T * G * N + states + B * H * c * 2,
         "state_pass": 2 * states + B * H * c * 2 + B * H * P * N * 5,
         "chunk_scan": 2 * T * H * P * sx + T * H * 4 + T * G * N + states + cb_causal,
+    }
+
+
+def algorithmic_ops(cfg):
+    """Algorithmic MFMA work per launch (multiply + add = 2 ops), causal products counted over
+    i <= j only: {kernel: (int8 ops, fp16 flops)}."""
+    B, L, H, P, G, N, Q = (cfg.batch, cfg.seqlen, cfg.nheads, cfg.headdim, cfg.ngroups,
+                           cfg.dstate, cfg.chunk)
+    c = L // Q
+    pairs = Q * (Q + 1) // 2
+    return {
+        "chunk_bmm": (2 * B * c * G * pairs * N, 0),
+        "chunk_state": (2 * B * c * H * Q * P * N, 0),
+        "chunk_scan": (2 * B * c * H * Q * N * P, 2 * B * c * H * pairs * P),
     }
 
 
@@ -219,6 +235,15 @@ def main():
                   "GBps": round(abytes[n] / (per[n] * 1e-3) / 1e9, 1),
                   "hbm_frac": round(abytes[n] / (per[n] * 1e-3) / 1e9 / HBM_PEAK_GBS, 3)}
               for n in names}
+    # MFMA utilisation of the contraction kernels (these shapes sit far below the machine
+    # balance, so the HBM fraction is the binding one; reported for completeness)
+    for n, (i8, f16) in algorithmic_ops(cfg).items():
+        sec = per[n] * 1e-3
+        stages[n]["int8_tops"] = round(i8 / sec / 1e12, 1)
+        stages[n]["int8_mfma_frac"] = round(i8 / sec / 1e12 / INT8_PEAK_TOPS, 4)
+        if f16:
+            stages[n]["fp16_tflops"] = round(f16 / sec / 1e12, 1)
+            stages[n]["fp16_mfma_frac"] = round(f16 / sec / 1e12 / FP16_PEAK_TFLOPS, 4)
     dom = "chunk_scan"
     ach = abytes[dom] / (per[dom] * 1e-3) / 1e9
     tokens = cfg.batch * cfg.seqlen

@@ -2,9 +2,9 @@
 //   P_in[0] = init;  P_in[c+1] = clamp(S_q[c] + ((q_d[c] P_in[c] + r) >> k), -127, 127)
 // The recurrence is sequential in c but independent per (batch, head, p, n) element, so each
 // thread owns 16 (or 4) consecutive int8 elements of one (b, h) slab and walks the chunks.  The
-// loads of S_q and q_d do not depend on the running state, so they are issued kDepth chunks
-// ahead (one batch of independent loads, then the dependent integer updates): the kernel is
-// bound by HBM bandwidth (read S_q, write P_in), not by the length of the chain.
+// loads of S_q and q_d do not depend on the running state, so they are issued in batches of
+// kDepth chunks, one batch ahead of the dependent integer updates: the kernel is bound by HBM
+// bandwidth (read S_q, write P_in), not by the length of the chain.
 //
 // Inside the SSD layer S_q and P_in are in the MFMA fragment order of frag.hpp (elementwise
 // work does not care); the initial state, the final states and the optional P_in tap are
@@ -76,16 +76,20 @@ __global__ __launch_bounds__(256) void state_pass_kernel(
   const size_t cstride = (size_t)H * elems;
   const size_t base = ((size_t)b * nc * H + h) * elems + off;
   const int16_t* qrow = qd + bh * nc;
-  for (int c0 = 0; c0 < nc; c0 += kDepth) {
-    uint32_t v[kDepth][kW];
-    int q[kDepth];
+  // batches of kDepth chunks; the loads of batch k+1 are issued before batch k is processed,
+  // so a long chunk sequence streams instead of waiting one load latency per batch
+  uint32_t v[2][kDepth][kW];
+  int q[2][kDepth];
+  auto load_batch = [&](int c0, int buf) {
 #pragma unroll
     for (int k = 0; k < kDepth; ++k) {
       if (c0 + k < nc) {
-        Vec<kW>::load(sq + base + (size_t)(c0 + k) * cstride, v[k]);
-        q[k] = qrow[c0 + k];
+        Vec<kW>::load(sq + base + (size_t)(c0 + k) * cstride, v[buf][k]);
+        q[buf][k] = qrow[c0 + k];
       }
     }
+  };
+  auto run_batch = [&](int c0, int buf) {
 #pragma unroll
     for (int k = 0; k < kDepth; ++k) {
       if (c0 + k < nc) {
@@ -97,8 +101,17 @@ __global__ __launch_bounds__(256) void state_pass_kernel(
         if (pin_tap) Vec<kW>::store(pin_tap + base - off + roff + (size_t)(c0 + k) * cstride, o);
 #pragma unroll
         for (int i = 0; i < kE; ++i)
-          st[i] = step_state(st[i], sext8(v[k][i >> 2], i & 3), q[k], shift, radd);
+          st[i] = step_state(st[i], sext8(v[buf][k][i >> 2], i & 3), q[buf][k], shift, radd);
       }
+    }
+  };
+  if (nc > 0) load_batch(0, 0);
+  for (int c0 = 0; c0 < nc; c0 += 2 * kDepth) {
+    if (c0 + kDepth < nc) load_batch(c0 + kDepth, 1);
+    run_batch(c0, 0);
+    if (c0 + kDepth < nc) {
+      if (c0 + 2 * kDepth < nc) load_batch(c0 + 2 * kDepth, 0);
+      run_batch(c0 + kDepth, 1);
     }
   }
   if (final_q) {
@@ -129,19 +142,25 @@ hipError_t launch_state_pass(int64_t batch, int64_t nchunks, int64_t nheads, int
                              int frag_k, hipStream_t st) {
   if (batch * nheads * elems == 0) return hipSuccess;
   const int radd = shift_round ? (1 << (shift - 1)) : 0;
-  // 16 elements per thread when a state row holds a multiple of 16 (they then share p)
-  const bool wide = (elems / headdim) % 16 == 0;
+  // 16 elements per thread when a state row holds a multiple of 16 (they then share p) and that
+  // still leaves at least 4 waves per CU; else 4 (long sequences of few heads are issue-bound:
+  // every thread walks all chunks)
+  const bool wide = (elems / headdim) % 16 == 0 && batch * nheads * elems / 16 >= 65536;
   const int64_t nthreads = batch * nheads * elems / (wide ? 16 : 4);
   const unsigned blocks = (unsigned)((nthreads + 255) / 256);
-#define SSDI8_PASS_LAUNCH(W, FK)                                                               \
-  hipLaunchKernelGGL((state_pass_kernel<8, W, FK>), dim3(blocks), dim3(256), 0, st, sq, qd,     \
+  // short sequences: one batch of 8 chunks covers them; long ones keep 2 x 16 chunks in flight
+  const bool deep = nchunks > 8;
+#define SSDI8_PASS_LAUNCH(D, W, FK)                                                            \
+  hipLaunchKernelGGL((state_pass_kernel<D, W, FK>), dim3(blocks), dim3(256), 0, st, sq, qd,     \
                      shift, radd, init, pin, pin_tap, final_q, final_state, state_scale,        \
                      (int)nchunks, (int)nheads, elems, headdim, nthreads)
   if (frag_k == kN && elems == (int64_t)kP * kN && headdim == kP) {
-    SSDI8_PASS_LAUNCH(4, kN);
+    if (!wide) SSDI8_PASS_LAUNCH(8, 1, kN);
+    else if (deep) SSDI8_PASS_LAUNCH(16, 4, kN);
+    else SSDI8_PASS_LAUNCH(8, 4, kN);
   } else if (frag_k == 0) {
-    if (wide) SSDI8_PASS_LAUNCH(4, 0);
-    else SSDI8_PASS_LAUNCH(1, 0);
+    if (wide) SSDI8_PASS_LAUNCH(8, 4, 0);
+    else SSDI8_PASS_LAUNCH(8, 1, 0);
   } else {
     return hipErrorInvalidValue;
   }
