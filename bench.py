@@ -124,6 +124,58 @@ def cpu_baseline(cfg, inp, sc, budget_s: float):
             "seconds": round(t, 2), "host_cpus": len(os.sched_getaffinity(0))}
 
 
+def time_decode(torch, ssdi8, cfg, inp, sc, K, W):
+    """One decode token for every (batch, head) of the workload (ssdi8_decode_step): one replay
+    of a graph of K chained steps after W warmup steps, bracketed by HIP events on the launch
+    stream; the int8 state stays in HBM.
+    Algorithmic bytes: the int8 state read and written, x and y, dt, the token's B_q and C_q."""
+    import numpy as np
+    Bt, H, P, G, N = cfg.batch, cfg.nheads, cfg.headdim, cfg.ngroups, cfg.dstate
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    f32 = lambda a: dev(np.asarray(a, np.float32))
+    x = dev(inp["x"][:, 0])
+    dt = f32(inp["dt_raw"][:, 0])
+    aB, aC, aXs, aS, aCB = (f32(sc[k]) for k in ("alpha_B", "alpha_C", "alpha_Xs", "alpha_S",
+                                                 "alpha_CB"))
+    Bq = ssdi8.quantize_act(dev(inp["B"][:, :1]), "group", aB)[0].reshape(Bt, G, N)
+    Cq = ssdi8.quantize_act(dev(inp["C"][:, :1]), "group", aC)[0].reshape(Bt, G, N)
+    A, D, corr = f32(inp["A"]), f32(inp["D"]), f32(sc["corr"])
+    state = torch.zeros((Bt, H, P, N), dtype=torch.int8, device="cuda")
+    y = torch.empty_like(x)
+    run = lambda: ssdi8.decode_step(x, dt, A, Bq, Cq, aB, aC, aXs, aS, aCB, state, D=D,
+                                    corr=corr, y=y)
+    for _ in range(W):
+        run()
+    torch.cuda.synchronize()
+    # K chained steps captured in one HIP graph (per-launch host overhead excluded, as in a
+    # captured serving loop); one replay is timed
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        run()
+    torch.cuda.current_stream().wait_stream(side)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for _ in range(K):
+            run()
+    graph.replay()
+    ev = ssdi8.HipEvents(2)
+    torch.cuda.synchronize()
+    ev.record(0)
+    graph.replay()
+    ev.record(1)
+    torch.cuda.synchronize()
+    us = ev.elapsed_ms(0, 1) / K * 1e3
+    ev.close()
+    sx = 2 if cfg.dtype == "fp16" else 4
+    nbytes = 2 * Bt * H * P * N + 2 * Bt * H * P * sx + 4 * Bt * H + 2 * Bt * G * N
+    gbs = nbytes / (us * 1e-6) / 1e9
+    return {"us": round(us, 2), "tokens_per_s": round(Bt / (us * 1e-6), 1),
+            "algorithmic_bytes": nbytes, "GBps": round(gbs, 1),
+            "hbm_frac": round(gbs / HBM_PEAK_GBS, 4),
+            "what": f"one decode token of {Bt} sequences x {H} heads (int8 state in place)"}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -266,6 +318,7 @@ def main():
         "layer_hbm_frac": round(layer_min_bytes(cfg) / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "stages": stages,
     }
+    result["decode"] = time_decode(torch, ssdi8, cfg, inp, sc, K, W)
     if args.copy_probe_mb > 0:
         n = args.copy_probe_mb << 20
         src = torch.ones(n, dtype=torch.uint8, device="cuda")

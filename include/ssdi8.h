@@ -169,6 +169,38 @@ size_t ssdi8_ssd_workspace_size(const ssdi8_dims* d);
  */
 ssdi8_status ssdi8_ssd_chunk_scan(const ssdi8_dims* d, const ssdi8_scan_args* a, void* stream);
 
+/*
+ * ssdi8_decode_step — one token of every (batch, head) sequence in the recurrent mode of the same
+ * persistent int8 state: the chunked method with a chunk of one token (Sec. 4.2; Eq. 7-9; Eq. 10
+ * correction at the SSD output).  With cs = dt·A:
+ *     q_d = rne(exp(cs)·2^k),  X_q = Q(fl32(dt·x) / a_X),  S_q = requant(X_q B_q^T, m_S)
+ *     y   = (C_q · state) a_C a_S exp(cs) + fp16(CB_q a_CB dt)·fp16(x) + D x + corr
+ *     state <- sat(S_q + ((q_d·state + r) >> k))
+ * where y reads the state entering the token.  The same scales as ssdi8_ssd_chunk_scan; B and C of
+ * the token are quantized first (ssdi8_quantize_act with l = 1).  Sizes as ssdi8_ssd_chunk_scan
+ * (headdim 64, dstate 128).  All device pointers; asynchronous on `stream`; no workspace.
+ */
+typedef struct {
+  const void* x; int x_dtype;         /* [B,H,P] the token's x, fp16 or fp32                     */
+  const float* dt; int dt_softplus;   /* [B,H]                                                    */
+  const float* A;                     /* [H]                                                      */
+  const int8_t* Bq; const int8_t* Cq; /* [B,G,N] the token's quantized B, C                       */
+  const float* B_scale;               /* [G]                                                      */
+  const float* C_scale;               /* [G], or [B,G] when c_per_token != 0                      */
+  int c_per_token;
+  const float* D;                     /* [H] or NULL (= 0)                                        */
+  const float* corr;                  /* [H,P] or NULL (= 0)                                      */
+  const float* xs_scale; int xs_per_head;   /* [H,P], or [H] when xs_per_head != 0             */
+  const float* state_scale;           /* [H,P]                                                    */
+  const float* cb_scale;              /* [G]                                                      */
+  int decay_shift; int shift_round;   /* k in [1, 14]; 1: add 2^(k-1) before the shift            */
+  int8_t* state_q;                    /* [B,H,P,N] in: state entering the token; out: after it    */
+  void* y; int y_dtype;               /* [B,H,P] output, fp16 or fp32                             */
+  float* state;                       /* [B,H,P,N] fp32 = new state_q * state_scale, or NULL      */
+} ssdi8_decode_args;
+ssdi8_status ssdi8_decode_step(int64_t batch, int64_t nheads, int64_t headdim, int64_t ngroups,
+                               int64_t dstate, const ssdi8_decode_args* a, void* stream);
+
 /* Static description of a status code. */
 const char* ssdi8_status_string(int status);
 

@@ -215,4 +215,30 @@ ssdi8_status ssdi8_ssd_chunk_scan(const ssdi8_dims* d, const ssdi8_scan_args* a,
   return SSDI8_OK;
 }
 
+ssdi8_status ssdi8_decode_step(int64_t batch, int64_t nheads, int64_t headdim, int64_t ngroups,
+                               int64_t dstate, const ssdi8_decode_args* a, void* stream) {
+  if (batch < 0 || nheads < 1 || headdim < 1 || ngroups < 1 || dstate < 1) return SSDI8_ERR_SHAPE;
+  if (batch >= kMaxDim || nheads >= kMaxDim || ngroups >= kMaxDim) return SSDI8_ERR_SHAPE;
+  if (nheads % ngroups != 0) return SSDI8_ERR_SHAPE;
+  if ((double)batch * nheads >= 2147483647.0) return SSDI8_ERR_SHAPE;
+  if (headdim != ssdi8::kP || dstate != ssdi8::kN) return SSDI8_ERR_UNSUPPORTED;
+  if (!a) return SSDI8_ERR_NULL;
+  if (a->x_dtype != SSDI8_F32 && a->x_dtype != SSDI8_F16) return SSDI8_ERR_ARG;
+  if (a->y_dtype != SSDI8_F32 && a->y_dtype != SSDI8_F16) return SSDI8_ERR_ARG;
+  if (a->decay_shift < 1 || a->decay_shift > 14) return SSDI8_ERR_ARG;
+  if (batch == 0) return SSDI8_OK;
+  if (!a->x || !a->dt || !a->A || !a->Bq || !a->Cq || !a->B_scale || !a->C_scale ||
+      !a->xs_scale || !a->state_scale || !a->cb_scale || !a->state_q || !a->y)
+    return SSDI8_ERR_NULL;
+  if (!aligned16(a->Bq) || !aligned16(a->Cq) || !aligned16(a->state_q) ||
+      !aligned16_or_null(a->state))
+    return SSDI8_ERR_ALIGN;
+  hipError_t e = ssdi8::launch_decode(
+      batch, nheads, ngroups, a->x, a->x_dtype, a->dt, a->dt_softplus, a->A, a->Bq, a->Cq,
+      a->B_scale, a->C_scale, a->c_per_token, a->D, a->corr, a->xs_scale, a->xs_per_head,
+      a->state_scale, a->cb_scale, a->decay_shift, a->shift_round, a->state_q, a->y, a->y_dtype,
+      a->state, (hipStream_t)stream);
+  return e == hipSuccess ? SSDI8_OK : SSDI8_ERR_HIP;
+}
+
 }  // extern "C"

@@ -52,4 +52,14 @@ hipError_t launch_chunk_scan(const LayerDims& d, const void* x, int x_dtype, con
                              const float* D, const float* corr, void* y, int y_dtype,
                              int32_t* y1_tap, hipStream_t st);
 
+// One-token decode step on the persistent int8 state (a chunk of one token), in place.
+hipError_t launch_decode(int64_t batch, int64_t nheads, int64_t ngroups, const void* x,
+                         int x_dtype, const float* dt, int dt_softplus, const float* A,
+                         const int8_t* Bq, const int8_t* Cq, const float* B_scale,
+                         const float* C_scale, int c_per_token, const float* D,
+                         const float* corr, const float* xs_scale, int xs_per_head,
+                         const float* state_scale, const float* cb_scale, int shift,
+                         int shift_round, int8_t* state, void* y, int y_dtype, float* state_f32,
+                         hipStream_t st);
+
 }  // namespace ssdi8

@@ -51,6 +51,16 @@ class ScanArgs(ctypes.Structure):
     ]
 
 
+class DecodeArgs(ctypes.Structure):
+    _fields_ = [
+        ("x", _P), ("x_dtype", _I), ("dt", _P), ("dt_softplus", _I), ("A", _P),
+        ("Bq", _P), ("Cq", _P), ("B_scale", _P), ("C_scale", _P), ("c_per_token", _I),
+        ("D", _P), ("corr", _P), ("xs_scale", _P), ("xs_per_head", _I), ("state_scale", _P),
+        ("cb_scale", _P), ("decay_shift", _I), ("shift_round", _I), ("state_q", _P),
+        ("y", _P), ("y_dtype", _I), ("state", _P),
+    ]
+
+
 _lib = None
 
 
@@ -73,6 +83,8 @@ def lib() -> ctypes.CDLL:
     L.ssdi8_ssd_workspace_size.restype = ctypes.c_size_t
     L.ssdi8_ssd_chunk_scan.argtypes = [ctypes.POINTER(Dims), ctypes.POINTER(ScanArgs), _P]
     L.ssdi8_ssd_chunk_scan.restype = _I
+    L.ssdi8_decode_step.argtypes = [i64, i64, i64, i64, i64, ctypes.POINTER(DecodeArgs), _P]
+    L.ssdi8_decode_step.restype = _I
     L.ssdi8_status_string.argtypes = [_I]
     L.ssdi8_status_string.restype = ctypes.c_char_p
     L.ssdi8_version.argtypes = []
@@ -274,6 +286,61 @@ def ssd_chunk_scan(x: torch.Tensor, dt: torch.Tensor, A: torch.Tensor, Bq: torch
         a.stage_events = ctypes.cast(stage_events, ctypes.c_void_p)
     st = lib().ssdi8_ssd_chunk_scan(ctypes.byref(d), ctypes.byref(a), _stream(stream))
     _check(st, "ssdi8_ssd_chunk_scan")
+    return out
+
+
+def decode_step(x: torch.Tensor, dt: torch.Tensor, A: torch.Tensor, Bq: torch.Tensor,
+                Cq: torch.Tensor, B_scale: torch.Tensor, C_scale: torch.Tensor,
+                xs_scale: torch.Tensor, state_scale: torch.Tensor, cb_scale: torch.Tensor,
+                state_q: torch.Tensor, *, D: Optional[torch.Tensor] = None,
+                corr: Optional[torch.Tensor] = None, dt_softplus: bool = True,
+                decay_shift: int = 7, shift_round: bool = True,
+                y_dtype: Optional[torch.dtype] = None, y: Optional[torch.Tensor] = None,
+                state_f32: bool = False, stream=None) -> Dict[str, torch.Tensor]:
+    """One decode token (ssdi8_decode_step): x (B,H,P), dt (B,H), Bq/Cq (B,G,N) int8, C_scale
+    (G) or (B,G); state_q (B,H,P,N) int8 is updated in place.  Returns y (B,H,P) and, with
+    state_f32, the dequantized new state."""
+    _need(x, "x")
+    B, H, P = x.shape
+    _need(Bq, "Bq", torch.int8)
+    G, N = Bq.shape[1], Bq.shape[2]
+    _need(Bq, "Bq", torch.int8, (B, G, N))
+    _need(Cq, "Cq", torch.int8, (B, G, N))
+    _need(dt, "dt", torch.float32, (B, H))
+    _need(A, "A", torch.float32, (H,))
+    _need(B_scale, "B_scale", torch.float32, (G,))
+    c_per_token = C_scale.dim() == 2
+    _need(C_scale, "C_scale", torch.float32, (B, G) if c_per_token else (G,))
+    xs_per_head = xs_scale.dim() == 1
+    _need(xs_scale, "xs_scale", torch.float32, (H,) if xs_per_head else (H, P))
+    _need(state_scale, "state_scale", torch.float32, (H, P))
+    _need(cb_scale, "cb_scale", torch.float32, (G,))
+    _need(state_q, "state_q", torch.int8, (B, H, P, N))
+    if D is not None:
+        _need(D, "D", torch.float32, (H,))
+    if corr is not None:
+        _need(corr, "corr", torch.float32, (H, P))
+    y_dtype = x.dtype if y_dtype is None else y_dtype
+    if y is None:
+        y = torch.empty((B, H, P), dtype=y_dtype, device=x.device)
+    _need(y, "y", y_dtype, (B, H, P))
+    a = DecodeArgs()
+    a.x, a.x_dtype = _ptr(x), _fdt(x)
+    a.dt, a.dt_softplus, a.A = _ptr(dt), int(dt_softplus), _ptr(A)
+    a.Bq, a.Cq, a.B_scale, a.C_scale = _ptr(Bq), _ptr(Cq), _ptr(B_scale), _ptr(C_scale)
+    a.c_per_token = int(c_per_token)
+    a.D, a.corr = _ptr(D), _ptr(corr)
+    a.xs_scale, a.xs_per_head = _ptr(xs_scale), int(xs_per_head)
+    a.state_scale, a.cb_scale = _ptr(state_scale), _ptr(cb_scale)
+    a.decay_shift, a.shift_round = int(decay_shift), int(shift_round)
+    a.state_q = _ptr(state_q)
+    a.y, a.y_dtype = _ptr(y), _fdt(y)
+    out: Dict[str, torch.Tensor] = {"y": y}
+    if state_f32:
+        out["state"] = torch.empty((B, H, P, N), dtype=torch.float32, device=x.device)
+        a.state = _ptr(out["state"])
+    st = lib().ssdi8_decode_step(B, H, P, G, N, ctypes.byref(a), _stream(stream))
+    _check(st, "ssdi8_decode_step")
     return out
 
 

@@ -61,6 +61,57 @@ def test_structs_match_the_header(ssdi8, tmp_path):
         assert getattr(ssdi8.ScanArgs, f).offset == off, f
 
 
+def test_decode_struct_matches_the_header(ssdi8, tmp_path):
+    fields = [f[0] for f in ssdi8.DecodeArgs._fields_]
+    src = tmp_path / "layout_dec.c"
+    lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "ssdi8.h"', 'int main(void) {',
+             'printf("%zu\\n", sizeof(ssdi8_decode_args));']
+    for f in fields:
+        lines.append(f'printf("%zu\\n", offsetof(ssdi8_decode_args, {f}));')
+    lines.append("return 0; }")
+    src.write_text("\n".join(lines))
+    exe = tmp_path / "layout_dec"
+    subprocess.run(["gcc", "-std=c11", "-I", os.path.join(ROOT, "include"), str(src), "-o",
+                    str(exe)], check=True)
+    vals = [int(v) for v in subprocess.run([str(exe)], capture_output=True, text=True,
+                                           check=True).stdout.split()]
+    assert vals[0] == ctypes.sizeof(ssdi8.DecodeArgs)
+    for f, off in zip(fields, vals[1:]):
+        assert getattr(ssdi8.DecodeArgs, f).offset == off, f
+
+
+def _decode_args(ssdi8, **over):
+    a = ssdi8.DecodeArgs()
+    for f in ("x", "dt", "A", "Bq", "Cq", "B_scale", "C_scale", "xs_scale", "state_scale",
+              "cb_scale", "state_q", "y"):
+        setattr(a, f, A16)
+    a.x_dtype = a.y_dtype = ssdi8.F16
+    a.decay_shift, a.shift_round, a.dt_softplus = 7, 1, 1
+    for k, v in over.items():
+        setattr(a, k, v)
+    return a
+
+
+def test_decode_argument_errors(ssdi8):
+    dec = ssdi8.lib().ssdi8_decode_step
+
+    def call(B=2, H=4, P=64, G=2, N=128, **over):
+        return dec(B, H, P, G, N, ctypes.byref(_decode_args(ssdi8, **over)), None)
+    assert dec(2, 4, 64, 2, 128, None, None) == ssdi8.ERR_NULL
+    for f in ("x", "dt", "A", "Bq", "Cq", "B_scale", "C_scale", "xs_scale", "state_scale",
+              "cb_scale", "state_q", "y"):
+        assert call(**{f: None}) == ssdi8.ERR_NULL, f
+    assert call(B=0, x=None) == ssdi8.OK                       # nothing to do
+    assert call(B=-1) == ssdi8.ERR_SHAPE
+    assert call(H=6, G=4) == ssdi8.ERR_SHAPE
+    assert call(P=32) == ssdi8.ERR_UNSUPPORTED
+    assert call(N=64) == ssdi8.ERR_UNSUPPORTED
+    assert call(decay_shift=0) == ssdi8.ERR_ARG
+    assert call(x_dtype=4) == ssdi8.ERR_ARG
+    assert call(Bq=A16 + 4) == ssdi8.ERR_ALIGN
+    assert call(state_q=A16 + 8) == ssdi8.ERR_ALIGN
+
+
 def test_status_strings_and_version(ssdi8):
     for s in range(8):
         assert ssdi8.status_string(s)

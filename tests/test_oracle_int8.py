@@ -233,10 +233,12 @@ def _exactness_preconditions(ref, CB_bound=127):
     assert np.abs(ref["entering"]).max() <= 127 and np.abs(ref["final_state"]).max() <= 127
 
 
+@pytest.mark.parametrize("Q", [16, 1])
 @pytest.mark.parametrize("seed", [0, 1, 2])
-def test_sc1_no_decay_is_exact(seed):
+def test_sc1_no_decay_is_exact(seed, Q):
+    # Q = 1 is the recurrent (decode) mode: every token is its own chunk
     x, dt, A, B, C, D = _special(seed)
-    H, P, G, Q = 2, 4, 1, 16
+    H, P, G = 2, 4, 1
     ref = exact.ssd_chunked(x, dt, A, B, C, D, Q)
     _exactness_preconditions(ref)
     out = int8.ssdi8_forward(x, dt, A, B, C, D, np.zeros((H, P), F32), _unit_scales(H, P, G),
@@ -251,9 +253,10 @@ def test_sc1_no_decay_is_exact(seed):
     assert np.array_equal(out["CBq"][:, :, 0], np.tril(CB))
 
 
-def test_sc1_with_initial_state_is_exact():
+@pytest.mark.parametrize("Q", [16, 1])
+def test_sc1_with_initial_state_is_exact(Q):
     x, dt, A, B, C, D = _special(7)
-    H, P, G, N, Q = 2, 4, 1, 8, 16
+    H, P, G, N = 2, 4, 1, 8
     rng = np.random.default_rng(8)
     init = rng.integers(-5, 6, (1, H, P, N)).astype(np.int8)
     ref = exact.ssd_chunked(x, dt, A, B, C, D, Q, init.astype(np.float64))
@@ -479,3 +482,32 @@ def test_fragile_tokens_are_rare():
     raw = rng.normal(-2, 0.5, 4096).astype(F32)
     bad = int8.fragile_tokens(raw, F32(-3.0), 256, True)
     assert bad.mean() < 0.01
+
+
+def test_decode_steps_chain_through_the_int8_state():
+    """The recurrent mode (a chunk of one token, Sec. 4.2 state passing with Eq. 9 per token):
+    T single-token calls chained through the final int8 state equal one call over T tokens
+    with chunk 1, stage by stage."""
+    rng = np.random.default_rng(21)
+    Bt, T, H, P, G, N = 2, 6, 4, 8, 2, 16
+    x = rng.standard_normal((Bt, T, H, P)).astype(np.float16)
+    dt_raw = rng.normal(-2, 0.5, (Bt, T, H)).astype(F32)
+    A = (-np.exp(rng.uniform(0, 2, H))).astype(F32)
+    B = rng.standard_normal((Bt, T, G, N)).astype(np.float16)
+    C = rng.standard_normal((Bt, T, G, N)).astype(np.float16)
+    D = rng.normal(1, 0.1, H).astype(F32)
+    corr = rng.normal(0, 0.1, (H, P)).astype(F32)
+    sc = _unit_scales(H, P, G, 0.02, 0.03, 0.03, 0.05, 0.1)
+    init = rng.integers(-60, 61, (Bt, H, P, N)).astype(np.int8)
+    whole = int8.ssdi8_forward(x, dt_raw, A, B, C, D, corr, sc, chunk=1, init_q=init,
+                               want=("y64", "final_q", "pin"))
+    state = init
+    for t in range(T):
+        one = int8.ssdi8_forward(x[:, t:t + 1], dt_raw[:, t:t + 1], A, B[:, t:t + 1],
+                                 C[:, t:t + 1], D, corr, sc, chunk=1, init_q=state,
+                                 want=("y64", "final_q", "pin"))
+        assert np.array_equal(one["pin"][:, 0], whole["pin"][:, t])
+        assert np.array_equal(one["y64"][:, 0], whole["y64"][:, t])
+        state = one["final_q"]
+    assert np.array_equal(state, whole["final_q"])
+    assert np.abs(whole["pin"].astype(int)).max() > 20        # the state is exercised
