@@ -124,6 +124,50 @@ def cpu_baseline(cfg, inp, sc, budget_s: float):
             "seconds": round(t, 2), "host_cpus": len(os.sched_getaffinity(0))}
 
 
+def time_fp16(torch, ssdi8, cfg, x, dt, A, Bf, Cf, D, K, W):
+    """The unquantized FP16 SSD layer on the same inputs (ssdi8_ssd_chunk_scan_fp16): K replays
+    of one captured graph for the step time, then K eager steps with stage events."""
+    ws = torch.empty(max(ssdi8.fp16_workspace_size(ssdi8.dims(cfg.batch, cfg.seqlen, cfg.nheads,
+                                                               cfg.ngroups)), 1),
+                     dtype=torch.uint8, device="cuda")
+    y = torch.empty_like(x)
+    ev = ssdi8.HipEvents(5 * max(K, 1))
+
+    def step(k=None):
+        ssdi8.ssd_chunk_scan_fp16(x, dt, A, Bf, Cf, D=D, workspace=ws, y=y, final_state=True,
+                                  stage_events=None if k is None else ev.group(5 * k))
+    for _ in range(W):
+        step()
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    graph.replay()
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for _ in range(K):
+        graph.replay()
+    t1.record()
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / K
+    for k in range(K):
+        step(k)
+    torch.cuda.synchronize()
+    names = ("chunk_bmm", "chunk_state", "state_pass", "chunk_scan")
+    per = {n: sum(ev.elapsed_ms(5 * k + i, 5 * k + i + 1) for k in range(K)) / K * 1e3
+           for i, n in enumerate(names)}
+    ev.close()
+    return {"ms_per_step": ms, "tokens_per_s": cfg.batch * cfg.seqlen / (ms * 1e-3),
+            "stages_us": {n: round(v, 2) for n, v in per.items()},
+            "what": "the same layer unquantized: fp16 operands, fp32 states (Alg. 2)"}
+
+
 def time_decode(torch, ssdi8, cfg, inp, sc, K, W):
     """One decode token for every (batch, head) of the workload (ssdi8_decode_step): one replay
     of a graph of K chained steps after W warmup steps, bracketed by HIP events on the launch
@@ -318,6 +362,9 @@ def main():
         "layer_hbm_frac": round(layer_min_bytes(cfg) / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "stages": stages,
     }
+    f16 = time_fp16(torch, ssdi8, cfg, x, dt, A, Bf, Cf, D, K, W)
+    f16["int8_speedup"] = round(value / f16["tokens_per_s"], 3)
+    result["fp16_baseline"] = f16
     result["decode"] = time_decode(torch, ssdi8, cfg, inp, sc, K, W)
     if args.copy_probe_mb > 0:
         n = args.copy_probe_mb << 20

@@ -201,6 +201,32 @@ typedef struct {
 ssdi8_status ssdi8_decode_step(int64_t batch, int64_t nheads, int64_t headdim, int64_t ngroups,
                                int64_t dstate, const ssdi8_decode_args* a, void* stream);
 
+/*
+ * ssdi8_ssd_chunk_scan_fp16 — the same SSD layer without quantization, as the FP16 baseline the
+ * paper's speedups are quoted against (Alg. 2 with fp16 contraction operands, fp32 accumulation
+ * and fp32 chunk states):
+ *     S = fp16(LUT_state·x)^T B,  P_in[c+1] = exp(cs_last) P_in[c] + S[c],
+ *     y = (C · fp16(P_in)) exp(cs) + fp16(C B^T · dt · exp(segsum)) · x + D x
+ * Sizes as ssdi8_ssd_chunk_scan; B and C are the unquantized fp16 (or fp32) tensors.  Scratch
+ * goes through `workspace` (ssdi8_fp16_workspace_size); stage_events as in ssdi8_scan_args.
+ */
+typedef struct {
+  const void* x; int x_dtype;         /* [B,L,H,P] fp16 or fp32                                   */
+  const float* dt; int dt_softplus;   /* [B,L,H]                                                  */
+  const float* A;                     /* [H]                                                      */
+  const void* B; const void* C;       /* [B,L,G,N]                                                */
+  int bc_dtype;                       /* dtype of B and C: SSDI8_F16 or SSDI8_F32                 */
+  const float* D;                     /* [H] or NULL (= 0)                                        */
+  const float* init_state;            /* [B,H,P,N] fp32 initial state, or NULL (= 0)              */
+  void* y; int y_dtype;               /* [B,L,H,P] output, fp16 or fp32                           */
+  float* final_state;                 /* [B,H,P,N] fp32, or NULL                                  */
+  void* workspace; size_t workspace_bytes;
+  void* const* stage_events;          /* NULL or 5 hipEvent_t (see ssdi8_scan_args)               */
+} ssdi8_fp16_args;
+size_t ssdi8_fp16_workspace_size(const ssdi8_dims* d);
+ssdi8_status ssdi8_ssd_chunk_scan_fp16(const ssdi8_dims* d, const ssdi8_fp16_args* a,
+                                       void* stream);
+
 /* Static description of a status code. */
 const char* ssdi8_status_string(int status);
 

@@ -13,6 +13,8 @@ Modules
   int8       the quantized SSDi8 path, stage by stage (Eq. 1, Sec. 4.2 with Eq. 7-9, Eq. 10).
   calibrate  static symmetric scale calibration and the single-layer mean correction
              (Sec. 5 setup, Eq. 10, Alg. 1 restricted to one layer).
+  fp16       the unquantized FP16 SSD (Alg. 2 with fp16 operands, fp32 states), the reference
+             of the on-box FP16 baseline the paper's speedups are measured against.
 
 Parity status: every function is pinned by the CPU tests in tests/test_oracle_*.py (brute-force
 equality of the three fp64 forms, exact special cases of the quantized path, integer closed

@@ -43,6 +43,28 @@ Plan plan_workspace(const ssdi8_dims* d) {
   return p;
 }
 
+struct Fp16Plan {
+  size_t bT, c16, S, pin, cb, dec, total;
+};
+
+// FP16-baseline workspace: fp16 B^T and C fragments per chunk, fp32 chunk states and entering
+// states (fragment order), fp32 causal CB blocks, fp32 per-chunk decays.
+Fp16Plan plan_fp16(const ssdi8_dims* d) {
+  const size_t B = (size_t)d->batch, L = (size_t)d->seqlen, H = (size_t)d->nheads;
+  const size_t P = (size_t)d->headdim, G = (size_t)d->ngroups, N = (size_t)d->dstate;
+  const size_t nc = L / (size_t)d->chunk;
+  Fp16Plan p;
+  size_t off = 0;
+  p.bT = off;  off = round_up(off + 2 * B * L * G * N, 256);
+  p.c16 = off; off = round_up(off + 2 * B * L * G * N, 256);
+  p.S = off;   off = round_up(off + 4 * B * nc * H * P * N, 256);
+  p.pin = off; off = round_up(off + 4 * B * nc * H * P * N, 256);
+  p.cb = off;  off = round_up(off + 4 * B * nc * G * (size_t)ssdi8::frag::kCbBlocks * 1024, 256);
+  p.dec = off; off = round_up(off + 4 * B * H * nc, 256);
+  p.total = off;
+  return p;
+}
+
 ssdi8_status check_dims(const ssdi8_dims* d) {
   if (!d) return SSDI8_ERR_NULL;
   if (d->batch < 0 || d->seqlen < 0 || d->nheads < 1 || d->headdim < 1 || d->ngroups < 1 ||
@@ -211,6 +233,71 @@ ssdi8_status ssdi8_ssd_chunk_scan(const ssdi8_dims* d, const ssdi8_scan_args* a,
   e = ssdi8::launch_chunk_scan(ld, a->x, a->x_dtype, a->dt, a->dt_softplus, a->A, cq,
                                a->C_scale, a->c_per_token, pin, cbq, a->cb_scale, a->state_scale,
                                a->D, a->corr, a->y, a->y_dtype, a->scan1_i32, st);
+  if (e != hipSuccess || !mark(4)) return SSDI8_ERR_HIP;
+  return SSDI8_OK;
+}
+
+size_t ssdi8_fp16_workspace_size(const ssdi8_dims* d) {
+  if (check_dims(d) != SSDI8_OK) return 0;
+  return plan_fp16(d).total;
+}
+
+ssdi8_status ssdi8_ssd_chunk_scan_fp16(const ssdi8_dims* d, const ssdi8_fp16_args* a,
+                                       void* stream) {
+  ssdi8_status s = check_dims(d);
+  if (s != SSDI8_OK) return s;
+  if (!a) return SSDI8_ERR_NULL;
+  if (a->x_dtype != SSDI8_F32 && a->x_dtype != SSDI8_F16) return SSDI8_ERR_ARG;
+  if (a->y_dtype != SSDI8_F32 && a->y_dtype != SSDI8_F16) return SSDI8_ERR_ARG;
+  if (a->bc_dtype != SSDI8_F32 && a->bc_dtype != SSDI8_F16) return SSDI8_ERR_ARG;
+  const bool work = d->batch > 0 && d->seqlen > 0;
+  if (work && (!a->x || !a->dt || !a->A || !a->B || !a->C || !a->y)) return SSDI8_ERR_NULL;
+  const void* al[] = {a->x, a->y, a->B, a->C, a->init_state, a->final_state, a->workspace};
+  for (const void* p : al)
+    if (!aligned16_or_null(p)) return SSDI8_ERR_ALIGN;
+  const Fp16Plan plan = plan_fp16(d);
+  if (work && (!a->workspace || a->workspace_bytes < plan.total)) return SSDI8_ERR_WORKSPACE;
+  if (a->stage_events)
+    for (int i = 0; i < 5; ++i)
+      if (!a->stage_events[i]) return SSDI8_ERR_NULL;
+  hipStream_t st = (hipStream_t)stream;
+  LayerDims ld;
+  ld.batch = (int)d->batch;
+  ld.seqlen = (int)d->seqlen;
+  ld.nheads = (int)d->nheads;
+  ld.ngroups = (int)d->ngroups;
+  ld.nchunks = (int)(d->seqlen / d->chunk);
+  if (!work) {
+    if (d->batch > 0 && a->final_state) {
+      // no tokens: the final state is the initial state (a pass over zero chunks)
+      ld.nchunks = 0;
+      hipError_t e = ssdi8::launch_fp16_pass(ld, nullptr, nullptr, a->init_state, nullptr,
+                                             a->final_state, st);
+      if (e != hipSuccess) return SSDI8_ERR_HIP;
+    }
+    return SSDI8_OK;
+  }
+  char* ws = static_cast<char*>(a->workspace);
+  _Float16* bT = reinterpret_cast<_Float16*>(ws + plan.bT);
+  _Float16* c16 = reinterpret_cast<_Float16*>(ws + plan.c16);
+  float* S = reinterpret_cast<float*>(ws + plan.S);
+  float* pin = reinterpret_cast<float*>(ws + plan.pin);
+  float* cb = reinterpret_cast<float*>(ws + plan.cb);
+  float* dec = reinterpret_cast<float*>(ws + plan.dec);
+  auto mark = [&](int i) -> bool {
+    return !a->stage_events ||
+           hipEventRecord(static_cast<hipEvent_t>(a->stage_events[i]), st) == hipSuccess;
+  };
+  if (!mark(0)) return SSDI8_ERR_HIP;
+  hipError_t e = ssdi8::launch_fp16_bmm(ld, a->C, a->B, a->bc_dtype, cb, bT, c16, st);
+  if (e != hipSuccess || !mark(1)) return SSDI8_ERR_HIP;
+  e = ssdi8::launch_fp16_state(ld, a->x, a->x_dtype, a->dt, a->dt_softplus, a->A, bT, S, dec,
+                               st);
+  if (e != hipSuccess || !mark(2)) return SSDI8_ERR_HIP;
+  e = ssdi8::launch_fp16_pass(ld, S, dec, a->init_state, pin, a->final_state, st);
+  if (e != hipSuccess || !mark(3)) return SSDI8_ERR_HIP;
+  e = ssdi8::launch_fp16_scan(ld, a->x, a->x_dtype, a->dt, a->dt_softplus, a->A, c16, pin, cb,
+                              a->D, a->y, a->y_dtype, st);
   if (e != hipSuccess || !mark(4)) return SSDI8_ERR_HIP;
   return SSDI8_OK;
 }

@@ -1,4 +1,4 @@
-// MFMA fragment order of the int8 tensors that one kernel writes and a later one reads as MFMA
+// MFMA fragment order of the tensors that one kernel writes and a later one reads as MFMA
 // operands (workspace only; the public tensors and debug taps keep their row-major layouts).
 //
 // An int8 operand of v_mfma_i32_32x32x32_i8 is a 32-row tile with a 32-wide K block; lane l
@@ -44,6 +44,23 @@ __host__ __device__ __forceinline__ int cb_block(int J, int I) { return J * (J +
 // Byte offset of in-block element (jj, ii) (0 <= jj, ii < 32) within its 1 KB CB block.
 __host__ __device__ __forceinline__ int cb_inblock(int jj, int ii) {
   return (jj + 32 * ((ii >> 3) & 1)) * 16 + (ii >> 4) * 8 + (ii & 7);
+}
+
+// fp16 operands of v_mfma_f32_32x32x16_f16 (and the fp32 states they are converted from): a
+// 32-row x 16-K tile of 512 elements, lane l holding row l % 32 and the 8 K values starting at
+// 8 (l / 32).  Element offset of (row, k) of a rows x K matrix (K % 16 == 0).
+__host__ __device__ __forceinline__ size_t k16_offset(int row, int k, int K) {
+  const int lane = (row & 31) + 32 * ((k & 15) >> 3);
+  return ((size_t)(row >> 5) * (K >> 4) + (k >> 4)) * 512 + lane * 8 + (k & 7);
+}
+
+// Inverse of k16_offset.
+__host__ __device__ __forceinline__ void k16_coords(size_t off, int K, int* row, int* k) {
+  const size_t tile = off >> 9;
+  const int kt = K >> 4;
+  const int lane = (int)((off >> 3) & 63);
+  *row = (int)(tile / kt) * 32 + (lane & 31);
+  *k = (int)(tile % kt) * 16 + 8 * (lane >> 5) + (int)(off & 7);
 }
 
 }  // namespace frag

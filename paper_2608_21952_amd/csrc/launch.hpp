@@ -62,4 +62,18 @@ hipError_t launch_decode(int64_t batch, int64_t nheads, int64_t ngroups, const v
                          int shift_round, int8_t* state, void* y, int y_dtype, float* state_f32,
                          hipStream_t st);
 
+// FP16 baseline: ChunkBMM (fp32 CB blocks, fp16 B^T and C fragments), ChunkState (fp32 states,
+// per-chunk decay), fp32 state passing, ChunkScan.
+hipError_t launch_fp16_bmm(const LayerDims& d, const void* C, const void* B, int dtype,
+                           float* cb_frag, _Float16* bT_frag, _Float16* c_frag, hipStream_t st);
+hipError_t launch_fp16_state(const LayerDims& d, const void* x, int x_dtype, const float* dt,
+                             int dt_softplus, const float* A, const _Float16* bT_frag, float* S,
+                             float* dec, hipStream_t st);
+hipError_t launch_fp16_pass(const LayerDims& d, const float* S, const float* dec,
+                            const float* init, float* pin, float* final_state, hipStream_t st);
+hipError_t launch_fp16_scan(const LayerDims& d, const void* x, int x_dtype, const float* dt,
+                            int dt_softplus, const float* A, const _Float16* c_frag,
+                            const float* pin, const float* cb, const float* D, void* y,
+                            int y_dtype, hipStream_t st);
+
 }  // namespace ssdi8

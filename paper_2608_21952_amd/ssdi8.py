@@ -61,6 +61,15 @@ class DecodeArgs(ctypes.Structure):
     ]
 
 
+class Fp16Args(ctypes.Structure):
+    _fields_ = [
+        ("x", _P), ("x_dtype", _I), ("dt", _P), ("dt_softplus", _I), ("A", _P),
+        ("B", _P), ("C", _P), ("bc_dtype", _I), ("D", _P), ("init_state", _P),
+        ("y", _P), ("y_dtype", _I), ("final_state", _P),
+        ("workspace", _P), ("workspace_bytes", ctypes.c_size_t), ("stage_events", _P),
+    ]
+
+
 _lib = None
 
 
@@ -85,6 +94,10 @@ def lib() -> ctypes.CDLL:
     L.ssdi8_ssd_chunk_scan.restype = _I
     L.ssdi8_decode_step.argtypes = [i64, i64, i64, i64, i64, ctypes.POINTER(DecodeArgs), _P]
     L.ssdi8_decode_step.restype = _I
+    L.ssdi8_fp16_workspace_size.argtypes = [ctypes.POINTER(Dims)]
+    L.ssdi8_fp16_workspace_size.restype = ctypes.c_size_t
+    L.ssdi8_ssd_chunk_scan_fp16.argtypes = [ctypes.POINTER(Dims), ctypes.POINTER(Fp16Args), _P]
+    L.ssdi8_ssd_chunk_scan_fp16.restype = _I
     L.ssdi8_status_string.argtypes = [_I]
     L.ssdi8_status_string.restype = ctypes.c_char_p
     L.ssdi8_version.argtypes = []
@@ -287,6 +300,60 @@ def ssd_chunk_scan(x: torch.Tensor, dt: torch.Tensor, A: torch.Tensor, Bq: torch
     st = lib().ssdi8_ssd_chunk_scan(ctypes.byref(d), ctypes.byref(a), _stream(stream))
     _check(st, "ssdi8_ssd_chunk_scan")
     return out
+
+
+def ssd_chunk_scan_fp16(x: torch.Tensor, dt: torch.Tensor, A: torch.Tensor, B: torch.Tensor,
+                        C: torch.Tensor, *, D: Optional[torch.Tensor] = None,
+                        dt_softplus: bool = True, chunk: int = CHUNK,
+                        init_state: Optional[torch.Tensor] = None,
+                        y_dtype: Optional[torch.dtype] = None, final_state: bool = True,
+                        workspace: Optional[torch.Tensor] = None,
+                        y: Optional[torch.Tensor] = None, stage_events=None,
+                        stream=None) -> Dict[str, torch.Tensor]:
+    """The unquantized FP16 SSD layer (ssdi8_ssd_chunk_scan_fp16), the baseline of the INT8
+    path.  x (B,L,H,P), dt (B,L,H), A (H), B/C (B,L,G,N) fp16 or fp32, D (H), init_state
+    (B,H,P,N) fp32.  Returns y and, with final_state, the fp32 final state."""
+    _need(x, "x")
+    Bt, L, H, P = x.shape
+    _need(B, "B")
+    G, N = B.shape[2], B.shape[3]
+    _need(B, "B", B.dtype, (Bt, L, G, N))
+    _need(C, "C", B.dtype, (Bt, L, G, N))
+    _need(dt, "dt", torch.float32, (Bt, L, H))
+    _need(A, "A", torch.float32, (H,))
+    if D is not None:
+        _need(D, "D", torch.float32, (H,))
+    if init_state is not None:
+        _need(init_state, "init_state", torch.float32, (Bt, H, P, N))
+    dev = x.device
+    y_dtype = x.dtype if y_dtype is None else y_dtype
+    if y is None:
+        y = torch.empty((Bt, L, H, P), dtype=y_dtype, device=dev)
+    _need(y, "y", y_dtype, (Bt, L, H, P))
+    d = dims(Bt, L, H, G, P, N, chunk)
+    need = lib().ssdi8_fp16_workspace_size(ctypes.byref(d))
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    a = Fp16Args()
+    a.x, a.x_dtype = _ptr(x), _fdt(x)
+    a.dt, a.dt_softplus, a.A = _ptr(dt), int(dt_softplus), _ptr(A)
+    a.B, a.C, a.bc_dtype = _ptr(B), _ptr(C), _fdt(B)
+    a.D, a.init_state = _ptr(D), _ptr(init_state)
+    a.y, a.y_dtype = _ptr(y), _fdt(y)
+    out: Dict[str, torch.Tensor] = {"y": y}
+    if final_state:
+        out["final_state"] = torch.empty((Bt, H, P, N), dtype=torch.float32, device=dev)
+        a.final_state = _ptr(out["final_state"])
+    a.workspace, a.workspace_bytes = _ptr(workspace), workspace.numel()
+    if stage_events is not None:
+        a.stage_events = ctypes.cast(stage_events, ctypes.c_void_p)
+    st = lib().ssdi8_ssd_chunk_scan_fp16(ctypes.byref(d), ctypes.byref(a), _stream(stream))
+    _check(st, "ssdi8_ssd_chunk_scan_fp16")
+    return out
+
+
+def fp16_workspace_size(d: Dims) -> int:
+    return int(lib().ssdi8_fp16_workspace_size(ctypes.byref(d)))
 
 
 def decode_step(x: torch.Tensor, dt: torch.Tensor, A: torch.Tensor, Bq: torch.Tensor,

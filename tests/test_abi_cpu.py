@@ -61,6 +61,56 @@ def test_structs_match_the_header(ssdi8, tmp_path):
         assert getattr(ssdi8.ScanArgs, f).offset == off, f
 
 
+def test_fp16_struct_matches_the_header(ssdi8, tmp_path):
+    fields = [f[0] for f in ssdi8.Fp16Args._fields_]
+    src = tmp_path / "layout_f16.c"
+    lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "ssdi8.h"', 'int main(void) {',
+             'printf("%zu\\n", sizeof(ssdi8_fp16_args));']
+    for f in fields:
+        lines.append(f'printf("%zu\\n", offsetof(ssdi8_fp16_args, {f}));')
+    lines.append("return 0; }")
+    src.write_text("\n".join(lines))
+    exe = tmp_path / "layout_f16"
+    subprocess.run(["gcc", "-std=c11", "-I", os.path.join(ROOT, "include"), str(src), "-o",
+                    str(exe)], check=True)
+    vals = [int(v) for v in subprocess.run([str(exe)], capture_output=True, text=True,
+                                           check=True).stdout.split()]
+    assert vals[0] == ctypes.sizeof(ssdi8.Fp16Args)
+    for f, off in zip(fields, vals[1:]):
+        assert getattr(ssdi8.Fp16Args, f).offset == off, f
+
+
+def test_fp16_argument_errors_and_workspace(ssdi8):
+    L = ssdi8.lib()
+    d = ssdi8.dims(2, 512, 8, 2)
+    B, Lq, H, P, G, N, c = 2, 512, 8, 64, 2, 128, 2
+    need = (2 * 2 * B * Lq * G * N + 2 * 4 * B * c * H * P * N + 4 * B * c * G * 36 * 1024
+            + 4 * B * H * c)
+    ws = ssdi8.fp16_workspace_size(d)
+    assert need <= ws <= need + 6 * 256
+    a = ssdi8.Fp16Args()
+    for f in ("x", "dt", "A", "B", "C", "y", "workspace"):
+        setattr(a, f, A16)
+    a.x_dtype = a.y_dtype = a.bc_dtype = ssdi8.F16
+    a.workspace_bytes = 1 << 40
+    call = lambda dd, aa: L.ssdi8_ssd_chunk_scan_fp16(ctypes.byref(dd), ctypes.byref(aa), None)
+    for f in ("x", "dt", "A", "B", "C", "y"):
+        old = getattr(a, f)
+        setattr(a, f, None)
+        assert call(d, a) == ssdi8.ERR_NULL, f
+        setattr(a, f, old)
+    a.bc_dtype = 3
+    assert call(d, a) == ssdi8.ERR_ARG
+    a.bc_dtype = ssdi8.F16
+    a.workspace_bytes = 16
+    assert call(d, a) == ssdi8.ERR_WORKSPACE
+    a.workspace_bytes = 1 << 40
+    a.B = A16 + 8
+    assert call(d, a) == ssdi8.ERR_ALIGN
+    a.B = A16
+    assert call(ssdi8.dims(2, 300, 8, 2), a) == ssdi8.ERR_SHAPE
+
+
 def test_decode_struct_matches_the_header(ssdi8, tmp_path):
     fields = [f[0] for f in ssdi8.DecodeArgs._fields_]
     src = tmp_path / "layout_dec.c"
