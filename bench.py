@@ -168,6 +168,28 @@ def time_fp16(torch, ssdi8, cfg, x, dt, A, Bf, Cf, D, K, W):
             "what": "the same layer unquantized: fp16 operands, fp32 states (Alg. 2)"}
 
 
+def time_calibrate(torch, ssdi8, cfg, x, dt, A, Bf, Cf, D, K):
+    """One static calibration of the workload on the device (ssdi8_calibrate: the steps of B, C,
+    X_scaled, the states and C.B^T, then the FP16 and the INT8 layer and the mean correction),
+    after one warmup call; K calls bracketed by events on the launch stream."""
+    d = ssdi8.dims(cfg.batch, cfg.seqlen, cfg.nheads, cfg.ngroups)
+    ws = torch.empty(max(ssdi8.calibrate_workspace_size(d), 1), dtype=torch.uint8, device="cuda")
+    call = lambda: ssdi8.calibrate(x, dt, A, Bf, Cf, D=D, xs_per_head=cfg.xs_per_head,
+                                   workspace=ws)
+    call()
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for _ in range(K):
+        call()
+    t1.record()
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / K
+    return {"ms_per_call": round(ms, 3), "tokens_per_s": cfg.batch * cfg.seqlen / (ms * 1e-3),
+            "calls": K, "workspace_MB": round(ws.numel() / 2**20, 1),
+            "what": "static steps + single-layer mean correction from this draw, on the device"}
+
+
 def time_decode(torch, ssdi8, cfg, inp, sc, K, W):
     """One decode token for every (batch, head) of the workload (ssdi8_decode_step): one replay
     of a graph of K chained steps after W warmup steps, bracketed by HIP events on the launch
@@ -366,6 +388,7 @@ def main():
     f16["int8_speedup"] = round(value / f16["tokens_per_s"], 3)
     result["fp16_baseline"] = f16
     result["decode"] = time_decode(torch, ssdi8, cfg, inp, sc, K, W)
+    result["calibrate"] = time_calibrate(torch, ssdi8, cfg, x, dt, A, Bf, Cf, D, min(K, 5))
     if args.copy_probe_mb > 0:
         n = args.copy_probe_mb << 20
         src = torch.ones(n, dtype=torch.uint8, device="cuda")

@@ -227,6 +227,47 @@ size_t ssdi8_fp16_workspace_size(const ssdi8_dims* d);
 ssdi8_status ssdi8_ssd_chunk_scan_fp16(const ssdi8_dims* d, const ssdi8_fp16_args* a,
                                        void* stream);
 
+/*
+ * ssdi8_calibrate — the static step sizes of ssdi8_ssd_chunk_scan and the per-channel mean
+ * correction, computed on the device from one calibration draw (Sec. 5 setup: symmetric static
+ * steps fixed offline; Eq. 10 / Alg. 1 for a single layer, damped by eta):
+ *     B_scale[g], C_scale[g]  fl32(absmax / 127) of B, C per group (Eq. 1)
+ *     xs_scale               fl32(absmax / 127) of X_scaled = fl32(LUT_state x) (Eq. 7), per
+ *                            (h, p) or per h; bit-identical to the values ChunkState quantizes
+ *     state_scale[h, p]      absmax over (b, c, n) of the chunk-local states (Eq. 4) and of the
+ *                            states after each chunk (passing in fp64), / 127
+ *     cb_scale[g]            absmax of the causal entries of C B^T over (b, c), / 127
+ *     corr[h, p]             eta * mean over (b, l) of (Y_fp - Y_q): Y_fp the FP16 layer
+ *                            (ssdi8_ssd_chunk_scan_fp16), Y_q the INT8 layer with the steps above,
+ *                            decay_shift / shift_round as given and no correction
+ * An absmax of 0 gives a step of 1.  The unquantized states are accumulated from
+ * X_scaled split into two fp16 parts (about 22 significant bits) times fp16 B with fp32 sums;
+ * C B^T uses fp16 C and B (fp32 inputs are rounded to fp16 there).  Sizes as ssdi8_ssd_chunk_scan;
+ * no initial state.  All device pointers, 16-byte aligned (the step outputs 4-byte); outputs are
+ * written, never read; asynchronous on `stream`; scratch through `workspace`
+ * (ssdi8_calibrate_workspace_size, about 8·B·L·H·P bytes more than the two layers' workspaces).
+ * Errors as ssdi8_ssd_chunk_scan; eta must be finite; B·L == 0 is SSDI8_ERR_SHAPE.
+ */
+typedef struct {
+  const void* x; int x_dtype;         /* [B,L,H,P] fp16 or fp32                                   */
+  const float* dt; int dt_softplus;   /* [B,L,H]                                                  */
+  const float* A;                     /* [H]                                                      */
+  const void* B; const void* C;       /* [B,L,G,N] unquantized                                    */
+  int bc_dtype;                       /* SSDI8_F16 or SSDI8_F32                                   */
+  const float* D;                     /* [H] or NULL (= 0)                                        */
+  int xs_per_head;                    /* 1: xs_scale is [H]; 0: [H,P]                             */
+  float eta;                          /* damping of the correction; the paper uses 0.15           */
+  int decay_shift; int shift_round;   /* of the INT8 layer that gives Y_q                         */
+  float* B_scale; float* C_scale;     /* [G] out                                                  */
+  float* xs_scale;                    /* [H,P] or [H] out                                         */
+  float* state_scale;                 /* [H,P] out                                                */
+  float* cb_scale;                    /* [G] out                                                  */
+  float* corr;                        /* [H,P] out                                                */
+  void* workspace; size_t workspace_bytes;
+} ssdi8_calib_args;
+size_t ssdi8_calibrate_workspace_size(const ssdi8_dims* d);
+ssdi8_status ssdi8_calibrate(const ssdi8_dims* d, const ssdi8_calib_args* a, void* stream);
+
 /* Static description of a status code. */
 const char* ssdi8_status_string(int status);
 

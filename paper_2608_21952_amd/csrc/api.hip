@@ -65,6 +65,35 @@ Fp16Plan plan_fp16(const ssdi8_dims* d) {
   return p;
 }
 
+struct CalibPlan {
+  Fp16Plan f16;
+  Plan i8;
+  size_t f16_base, i8_base, bq, cq, yfp, yq, dec64, amax, total;
+};
+
+// Calibration workspace: the FP16 layer's and the INT8 layer's workspaces, the quantized B and C,
+// the two fp32 outputs Y_fp and Y_q, the fp64 chunk decays, and the absmax words (x: H*P,
+// states: H*P, C.B^T: G).
+CalibPlan plan_calib(const ssdi8_dims* d) {
+  const size_t B = (size_t)d->batch, L = (size_t)d->seqlen, H = (size_t)d->nheads;
+  const size_t P = (size_t)d->headdim, G = (size_t)d->ngroups, N = (size_t)d->dstate;
+  const size_t nc = L / (size_t)d->chunk;
+  CalibPlan p;
+  p.f16 = plan_fp16(d);
+  p.i8 = plan_workspace(d);
+  size_t off = 0;
+  p.f16_base = off; off = round_up(off + p.f16.total, 256);
+  p.i8_base = off;  off = round_up(off + p.i8.total, 256);
+  p.bq = off;       off = round_up(off + B * L * G * N, 256);
+  p.cq = off;       off = round_up(off + B * L * G * N, 256);
+  p.yfp = off;      off = round_up(off + 4 * B * L * H * P, 256);
+  p.yq = off;       off = round_up(off + 4 * B * L * H * P, 256);
+  p.dec64 = off;    off = round_up(off + 8 * B * H * nc, 256);
+  p.amax = off;     off = round_up(off + 4 * (2 * H * P + G), 256);
+  p.total = off;
+  return p;
+}
+
 ssdi8_status check_dims(const ssdi8_dims* d) {
   if (!d) return SSDI8_ERR_NULL;
   if (d->batch < 0 || d->seqlen < 0 || d->nheads < 1 || d->headdim < 1 || d->ngroups < 1 ||
@@ -289,7 +318,7 @@ ssdi8_status ssdi8_ssd_chunk_scan_fp16(const ssdi8_dims* d, const ssdi8_fp16_arg
            hipEventRecord(static_cast<hipEvent_t>(a->stage_events[i]), st) == hipSuccess;
   };
   if (!mark(0)) return SSDI8_ERR_HIP;
-  hipError_t e = ssdi8::launch_fp16_bmm(ld, a->C, a->B, a->bc_dtype, cb, bT, c16, st);
+  hipError_t e = ssdi8::launch_fp16_bmm(ld, a->C, a->B, a->bc_dtype, cb, bT, c16, nullptr, st);
   if (e != hipSuccess || !mark(1)) return SSDI8_ERR_HIP;
   e = ssdi8::launch_fp16_state(ld, a->x, a->x_dtype, a->dt, a->dt_softplus, a->A, bT, S, dec,
                                st);
@@ -300,6 +329,114 @@ ssdi8_status ssdi8_ssd_chunk_scan_fp16(const ssdi8_dims* d, const ssdi8_fp16_arg
                               a->D, a->y, a->y_dtype, st);
   if (e != hipSuccess || !mark(4)) return SSDI8_ERR_HIP;
   return SSDI8_OK;
+}
+
+size_t ssdi8_calibrate_workspace_size(const ssdi8_dims* d) {
+  if (check_dims(d) != SSDI8_OK || d->batch == 0 || d->seqlen == 0) return 0;
+  return plan_calib(d).total;
+}
+
+ssdi8_status ssdi8_calibrate(const ssdi8_dims* d, const ssdi8_calib_args* a, void* stream) {
+  ssdi8_status s = check_dims(d);
+  if (s != SSDI8_OK) return s;
+  if (d->batch == 0 || d->seqlen == 0) return SSDI8_ERR_SHAPE;
+  if (!a) return SSDI8_ERR_NULL;
+  if (a->x_dtype != SSDI8_F32 && a->x_dtype != SSDI8_F16) return SSDI8_ERR_ARG;
+  if (a->bc_dtype != SSDI8_F32 && a->bc_dtype != SSDI8_F16) return SSDI8_ERR_ARG;
+  if (a->decay_shift < 1 || a->decay_shift > 14) return SSDI8_ERR_ARG;
+  if (!(a->eta == a->eta) || a->eta > 3.0e38f || a->eta < -3.0e38f) return SSDI8_ERR_ARG;
+  if (!a->x || !a->dt || !a->A || !a->B || !a->C || !a->B_scale || !a->C_scale ||
+      !a->xs_scale || !a->state_scale || !a->cb_scale || !a->corr)
+    return SSDI8_ERR_NULL;
+  const void* al[] = {a->x, a->B, a->C, a->workspace};
+  for (const void* p : al)
+    if (!aligned16_or_null(p)) return SSDI8_ERR_ALIGN;
+  const void* al4[] = {a->B_scale, a->C_scale, a->xs_scale, a->state_scale, a->cb_scale,
+                       a->corr};
+  for (const void* p : al4)
+    if (((uintptr_t)p & 3u) != 0) return SSDI8_ERR_ALIGN;
+  const CalibPlan plan = plan_calib(d);
+  if (!a->workspace || a->workspace_bytes < plan.total) return SSDI8_ERR_WORKSPACE;
+  if (ssdi8::quantize_max_granules() < d->ngroups) return SSDI8_ERR_UNSUPPORTED;
+
+  hipStream_t st = (hipStream_t)stream;
+  LayerDims ld;
+  ld.batch = (int)d->batch;
+  ld.seqlen = (int)d->seqlen;
+  ld.nheads = (int)d->nheads;
+  ld.ngroups = (int)d->ngroups;
+  ld.nchunks = (int)(d->seqlen / d->chunk);
+  const int H = (int)d->nheads, G = (int)d->ngroups, P = (int)d->headdim;
+  char* ws = static_cast<char*>(a->workspace);
+  char* f16 = ws + plan.f16_base;
+  _Float16* bT = reinterpret_cast<_Float16*>(f16 + plan.f16.bT);
+  _Float16* c16 = reinterpret_cast<_Float16*>(f16 + plan.f16.c16);
+  float* S = reinterpret_cast<float*>(f16 + plan.f16.S);
+  float* pin16 = reinterpret_cast<float*>(f16 + plan.f16.pin);
+  float* cb = reinterpret_cast<float*>(f16 + plan.f16.cb);
+  float* dec = reinterpret_cast<float*>(f16 + plan.f16.dec);
+  char* i8 = ws + plan.i8_base;
+  int8_t* bqT = reinterpret_cast<int8_t*>(i8 + plan.i8.bqT);
+  int8_t* cqf = reinterpret_cast<int8_t*>(i8 + plan.i8.cq);
+  int8_t* sq = reinterpret_cast<int8_t*>(i8 + plan.i8.sq);
+  int8_t* pin8 = reinterpret_cast<int8_t*>(i8 + plan.i8.pin);
+  int8_t* cbq = reinterpret_cast<int8_t*>(i8 + plan.i8.cbq);
+  int16_t* qd = reinterpret_cast<int16_t*>(i8 + plan.i8.qd);
+  int8_t* Bq = reinterpret_cast<int8_t*>(ws + plan.bq);
+  int8_t* Cq = reinterpret_cast<int8_t*>(ws + plan.cq);
+  float* yfp = reinterpret_cast<float*>(ws + plan.yfp);
+  float* yq = reinterpret_cast<float*>(ws + plan.yq);
+  double* dec64 = reinterpret_cast<double*>(ws + plan.dec64);
+  uint32_t* xs_amax = reinterpret_cast<uint32_t*>(ws + plan.amax);
+  uint32_t* s_amax = xs_amax + H * P;
+  uint32_t* cb_amax = s_amax + H * P;
+
+  // steps of B and C (dynamic per-group absmax), then the quantities the other steps are taken of
+  hipError_t e = ssdi8::launch_calib_zero(xs_amax, 2 * H * P + G, st);
+  if (e == hipSuccess)
+    e = ssdi8::launch_quantize(a->B, a->bc_dtype, d->batch, d->seqlen, d->ngroups, d->dstate,
+                               SSDI8_GRAN_GROUP, a->B_scale, 1, Bq, st);
+  if (e == hipSuccess)
+    e = ssdi8::launch_quantize(a->C, a->bc_dtype, d->batch, d->seqlen, d->ngroups, d->dstate,
+                               SSDI8_GRAN_GROUP, a->C_scale, 1, Cq, st);
+  if (e == hipSuccess)
+    e = ssdi8::launch_calib_xs(ld, a->x, a->x_dtype, a->dt, a->dt_softplus, a->A, xs_amax, st);
+  if (e == hipSuccess)
+    e = ssdi8::launch_fp16_bmm(ld, a->C, a->B, a->bc_dtype, cb, bT, c16, cb_amax, st);
+  if (e == hipSuccess)
+    e = ssdi8::launch_calib_states(ld, a->x, a->x_dtype, a->dt, a->dt_softplus, a->A, bT, S,
+                                   dec64, s_amax, st);
+  if (e == hipSuccess)
+    e = ssdi8::launch_calib_steps(xs_amax, s_amax, cb_amax, a->xs_scale, a->state_scale,
+                                  a->cb_scale, H, G, a->xs_per_head, st);
+  // Y_fp: the FP16 layer (its ChunkBMM outputs are already in place)
+  if (e == hipSuccess)
+    e = ssdi8::launch_fp16_state(ld, a->x, a->x_dtype, a->dt, a->dt_softplus, a->A, bT, S, dec,
+                                 st);
+  if (e == hipSuccess) e = ssdi8::launch_fp16_pass(ld, S, dec, nullptr, pin16, nullptr, st);
+  if (e == hipSuccess)
+    e = ssdi8::launch_fp16_scan(ld, a->x, a->x_dtype, a->dt, a->dt_softplus, a->A, c16, pin16,
+                                cb, a->D, yfp, SSDI8_F32, st);
+  // Y_q: the INT8 layer with the new steps and no correction
+  if (e == hipSuccess)
+    e = ssdi8::launch_chunk_bmm(ld, Cq, Bq, a->C_scale, 0, a->B_scale, a->cb_scale, cbq,
+                                nullptr, nullptr, bqT, cqf, st);
+  if (e == hipSuccess)
+    e = ssdi8::launch_chunk_state(ld, a->x, a->x_dtype, a->dt, a->dt_softplus, a->A, bqT,
+                                  a->B_scale, a->xs_scale, a->xs_per_head, a->state_scale,
+                                  a->decay_shift, sq, qd, nullptr, nullptr, nullptr, st);
+  if (e == hipSuccess)
+    e = ssdi8::launch_state_pass(d->batch, ld.nchunks, d->nheads, d->headdim * d->dstate,
+                                 d->headdim, sq, qd, a->decay_shift, a->shift_round, nullptr,
+                                 pin8, nullptr, nullptr, nullptr, a->state_scale,
+                                 (int)d->dstate, st);
+  if (e == hipSuccess)
+    e = ssdi8::launch_chunk_scan(ld, a->x, a->x_dtype, a->dt, a->dt_softplus, a->A, cqf,
+                                 a->C_scale, 0, pin8, cbq, a->cb_scale, a->state_scale, a->D,
+                                 nullptr, yq, SSDI8_F32, nullptr, st);
+  if (e == hipSuccess)
+    e = ssdi8::launch_calib_corr(yfp, yq, a->corr, d->batch * d->seqlen, H, a->eta, st);
+  return e == hipSuccess ? SSDI8_OK : SSDI8_ERR_HIP;
 }
 
 ssdi8_status ssdi8_decode_step(int64_t batch, int64_t nheads, int64_t headdim, int64_t ngroups,

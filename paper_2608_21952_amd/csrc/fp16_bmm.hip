@@ -41,7 +41,8 @@ __global__ __launch_bounds__(256) void fp16_bmm_kernel(const T* __restrict__ C,
                                                        const T* __restrict__ B,
                                                        float* __restrict__ cb_frag,
                                                        _Float16* __restrict__ bT_frag,
-                                                       _Float16* __restrict__ c_frag, int L,
+                                                       _Float16* __restrict__ c_frag,
+                                                       uint32_t* __restrict__ cb_amax, int L,
                                                        int G, int nc) {
   __shared__ __attribute__((aligned(16))) uint8_t smem[kHalfTok * kBRow];
 
@@ -134,22 +135,37 @@ __global__ __launch_bounds__(256) void fp16_bmm_kernel(const T* __restrict__ C,
                                           1024 + lane * 16);
 #pragma unroll
   for (int u = 0; u < 4; ++u) out[u] = o[u];
+  if (cb_amax) {
+    // calibration: absolute maximum of the causal entries of this group's C.B^T (the masked
+    // entries were staged as 0); bit patterns of non-negative floats order like the floats
+    float m = 0.0f;
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      m = __builtin_fmaxf(m, __builtin_fmaxf(__builtin_fmaxf(__builtin_fabsf(o[u].x),
+                                                             __builtin_fabsf(o[u].y)),
+                                             __builtin_fmaxf(__builtin_fabsf(o[u].z),
+                                                             __builtin_fabsf(o[u].w))));
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) m = __builtin_fmaxf(m, __shfl_xor(m, off, 64));
+    if (lane == 0) atomicMax(cb_amax + g, __float_as_uint(m));
+  }
 }
 
 }  // namespace
 
 hipError_t launch_fp16_bmm(const LayerDims& d, const void* C, const void* B, int dtype,
-                           float* cb_frag, _Float16* bT_frag, _Float16* c_frag, hipStream_t st) {
+                           float* cb_frag, _Float16* bT_frag, _Float16* c_frag,
+                           uint32_t* cb_amax, hipStream_t st) {
   const int64_t nwork = (int64_t)d.batch * d.nchunks * d.ngroups * kRoles;
   if (nwork == 0) return hipSuccess;
   if (dtype == 1)
     hipLaunchKernelGGL(fp16_bmm_kernel<_Float16>, dim3((unsigned)nwork), dim3(256), 0, st,
                        static_cast<const _Float16*>(C), static_cast<const _Float16*>(B),
-                       cb_frag, bT_frag, c_frag, d.seqlen, d.ngroups, d.nchunks);
+                       cb_frag, bT_frag, c_frag, cb_amax, d.seqlen, d.ngroups, d.nchunks);
   else
     hipLaunchKernelGGL(fp16_bmm_kernel<float>, dim3((unsigned)nwork), dim3(256), 0, st,
                        static_cast<const float*>(C), static_cast<const float*>(B), cb_frag,
-                       bT_frag, c_frag, d.seqlen, d.ngroups, d.nchunks);
+                       bT_frag, c_frag, cb_amax, d.seqlen, d.ngroups, d.nchunks);
   return hipGetLastError();
 }
 

@@ -65,7 +65,8 @@ hipError_t launch_decode(int64_t batch, int64_t nheads, int64_t ngroups, const v
 // FP16 baseline: ChunkBMM (fp32 CB blocks, fp16 B^T and C fragments), ChunkState (fp32 states,
 // per-chunk decay), fp32 state passing, ChunkScan.
 hipError_t launch_fp16_bmm(const LayerDims& d, const void* C, const void* B, int dtype,
-                           float* cb_frag, _Float16* bT_frag, _Float16* c_frag, hipStream_t st);
+                           float* cb_frag, _Float16* bT_frag, _Float16* c_frag,
+                           uint32_t* cb_amax, hipStream_t st);
 hipError_t launch_fp16_state(const LayerDims& d, const void* x, int x_dtype, const float* dt,
                              int dt_softplus, const float* A, const _Float16* bT_frag, float* S,
                              float* dec, hipStream_t st);
@@ -75,5 +76,20 @@ hipError_t launch_fp16_scan(const LayerDims& d, const void* x, int x_dtype, cons
                             int dt_softplus, const float* A, const _Float16* c_frag,
                             const float* pin, const float* cb, const float* D, void* y,
                             int y_dtype, hipStream_t st);
+
+// Calibration (static steps and the mean correction): absmax words cleared by a fill kernel,
+// absmax of X_scaled, fp states from split fp16 operands with their absmax, the steps, the
+// correction from two fp32 layer outputs.
+hipError_t launch_calib_zero(uint32_t* p, int n, hipStream_t st);
+hipError_t launch_calib_xs(const LayerDims& d, const void* x, int x_dtype, const float* dt,
+                           int dt_softplus, const float* A, uint32_t* xs_amax, hipStream_t st);
+hipError_t launch_calib_states(const LayerDims& d, const void* x, int x_dtype, const float* dt,
+                               int dt_softplus, const float* A, const _Float16* bT_frag,
+                               float* S, double* dec64, uint32_t* s_amax, hipStream_t st);
+hipError_t launch_calib_steps(const uint32_t* xs_amax, const uint32_t* s_amax,
+                              const uint32_t* cb_amax, float* aXs, float* aS, float* aCB, int H,
+                              int G, int xs_per_head, hipStream_t st);
+hipError_t launch_calib_corr(const float* y_fp, const float* y_q, float* corr, int64_t T, int H,
+                             float eta, hipStream_t st);
 
 }  // namespace ssdi8

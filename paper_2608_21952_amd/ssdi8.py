@@ -70,6 +70,17 @@ class Fp16Args(ctypes.Structure):
     ]
 
 
+class CalibArgs(ctypes.Structure):
+    _fields_ = [
+        ("x", _P), ("x_dtype", _I), ("dt", _P), ("dt_softplus", _I), ("A", _P),
+        ("B", _P), ("C", _P), ("bc_dtype", _I), ("D", _P), ("xs_per_head", _I),
+        ("eta", ctypes.c_float), ("decay_shift", _I), ("shift_round", _I),
+        ("B_scale", _P), ("C_scale", _P), ("xs_scale", _P), ("state_scale", _P),
+        ("cb_scale", _P), ("corr", _P),
+        ("workspace", _P), ("workspace_bytes", ctypes.c_size_t),
+    ]
+
+
 _lib = None
 
 
@@ -98,6 +109,10 @@ def lib() -> ctypes.CDLL:
     L.ssdi8_fp16_workspace_size.restype = ctypes.c_size_t
     L.ssdi8_ssd_chunk_scan_fp16.argtypes = [ctypes.POINTER(Dims), ctypes.POINTER(Fp16Args), _P]
     L.ssdi8_ssd_chunk_scan_fp16.restype = _I
+    L.ssdi8_calibrate_workspace_size.argtypes = [ctypes.POINTER(Dims)]
+    L.ssdi8_calibrate_workspace_size.restype = ctypes.c_size_t
+    L.ssdi8_calibrate.argtypes = [ctypes.POINTER(Dims), ctypes.POINTER(CalibArgs), _P]
+    L.ssdi8_calibrate.restype = _I
     L.ssdi8_status_string.argtypes = [_I]
     L.ssdi8_status_string.restype = ctypes.c_char_p
     L.ssdi8_version.argtypes = []
@@ -354,6 +369,52 @@ def ssd_chunk_scan_fp16(x: torch.Tensor, dt: torch.Tensor, A: torch.Tensor, B: t
 
 def fp16_workspace_size(d: Dims) -> int:
     return int(lib().ssdi8_fp16_workspace_size(ctypes.byref(d)))
+
+
+def calibrate(x: torch.Tensor, dt: torch.Tensor, A: torch.Tensor, B: torch.Tensor,
+              C: torch.Tensor, *, D: Optional[torch.Tensor] = None, dt_softplus: bool = True,
+              chunk: int = CHUNK, xs_per_head: bool = False, eta: float = 0.15,
+              decay_shift: int = 7, shift_round: bool = True,
+              workspace: Optional[torch.Tensor] = None, stream=None) -> Dict[str, torch.Tensor]:
+    """Static steps and the per-channel mean correction from one calibration draw
+    (ssdi8_calibrate).  Returns alpha_B, alpha_C (G), alpha_Xs (H,P) or (H), alpha_S (H,P),
+    alpha_CB (G) and corr (H,P), fp32 on the device of x."""
+    _need(x, "x")
+    Bt, L, H, P = x.shape
+    _need(B, "B")
+    G, N = B.shape[2], B.shape[3]
+    _need(B, "B", B.dtype, (Bt, L, G, N))
+    _need(C, "C", B.dtype, (Bt, L, G, N))
+    _need(dt, "dt", torch.float32, (Bt, L, H))
+    _need(A, "A", torch.float32, (H,))
+    if D is not None:
+        _need(D, "D", torch.float32, (H,))
+    dev = x.device
+    d = dims(Bt, L, H, G, P, N, chunk)
+    need = lib().ssdi8_calibrate_workspace_size(ctypes.byref(d))
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    f32 = lambda *s: torch.empty(s, dtype=torch.float32, device=dev)
+    out = {"alpha_B": f32(G), "alpha_C": f32(G),
+           "alpha_Xs": f32(H) if xs_per_head else f32(H, P), "alpha_S": f32(H, P),
+           "alpha_CB": f32(G), "corr": f32(H, P)}
+    a = CalibArgs()
+    a.x, a.x_dtype = _ptr(x), _fdt(x)
+    a.dt, a.dt_softplus, a.A = _ptr(dt), int(dt_softplus), _ptr(A)
+    a.B, a.C, a.bc_dtype, a.D = _ptr(B), _ptr(C), _fdt(B), _ptr(D)
+    a.xs_per_head, a.eta = int(xs_per_head), float(eta)
+    a.decay_shift, a.shift_round = int(decay_shift), int(shift_round)
+    a.B_scale, a.C_scale = _ptr(out["alpha_B"]), _ptr(out["alpha_C"])
+    a.xs_scale, a.state_scale = _ptr(out["alpha_Xs"]), _ptr(out["alpha_S"])
+    a.cb_scale, a.corr = _ptr(out["alpha_CB"]), _ptr(out["corr"])
+    a.workspace, a.workspace_bytes = _ptr(workspace), workspace.numel()
+    st = lib().ssdi8_calibrate(ctypes.byref(d), ctypes.byref(a), _stream(stream))
+    _check(st, "ssdi8_calibrate")
+    return out
+
+
+def calibrate_workspace_size(d: Dims) -> int:
+    return int(lib().ssdi8_calibrate_workspace_size(ctypes.byref(d)))
 
 
 def decode_step(x: torch.Tensor, dt: torch.Tensor, A: torch.Tensor, Bq: torch.Tensor,

@@ -269,3 +269,61 @@ def test_bench_refuses_more_than_one_gpu():
     r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
                        capture_output=True, text=True, timeout=120)
     assert r.returncode == 2 and "one GPU" in r.stderr
+
+
+def test_calib_struct_matches_the_header(ssdi8, tmp_path):
+    fields = [f[0] for f in ssdi8.CalibArgs._fields_]
+    src = tmp_path / "layout_cal.c"
+    lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "ssdi8.h"', 'int main(void) {',
+             'printf("%zu\\n", sizeof(ssdi8_calib_args));']
+    for f in fields:
+        lines.append(f'printf("%zu\\n", offsetof(ssdi8_calib_args, {f}));')
+    lines.append("return 0; }")
+    src.write_text("\n".join(lines))
+    exe = tmp_path / "layout_cal"
+    subprocess.run(["gcc", "-std=c11", "-I", os.path.join(ROOT, "include"), str(src), "-o",
+                    str(exe)], check=True)
+    vals = [int(v) for v in subprocess.run([str(exe)], capture_output=True, text=True,
+                                           check=True).stdout.split()]
+    assert vals[0] == ctypes.sizeof(ssdi8.CalibArgs)
+    for f, off in zip(fields, vals[1:]):
+        assert getattr(ssdi8.CalibArgs, f).offset == off, f
+
+
+def test_calib_argument_errors_and_workspace(ssdi8):
+    L = ssdi8.lib()
+    d = ssdi8.dims(2, 512, 8, 2)
+    B, Lq, H, P, G, N = 2, 512, 8, 64, 2, 128
+    ws = ssdi8.calibrate_workspace_size(d)
+    parts = (ssdi8.fp16_workspace_size(d) + ssdi8.workspace_size(d) + 2 * B * Lq * G * N
+             + 2 * 4 * B * Lq * H * P + 8 * B * H * 2 + 4 * (2 * H * P + G))
+    assert parts <= ws <= parts + 8 * 256
+    assert ssdi8.calibrate_workspace_size(ssdi8.dims(0, 512, 8, 2)) == 0
+    a = ssdi8.CalibArgs()
+    for f in ("x", "dt", "A", "B", "C", "B_scale", "C_scale", "xs_scale", "state_scale",
+              "cb_scale", "corr", "workspace"):
+        setattr(a, f, A16)
+    a.x_dtype = a.bc_dtype = ssdi8.F16
+    a.eta, a.decay_shift, a.shift_round = 0.15, 7, 1
+    a.workspace_bytes = 1 << 40
+    call = lambda dd, aa: L.ssdi8_calibrate(ctypes.byref(dd), ctypes.byref(aa), None)
+    for f in ("x", "dt", "A", "B", "C", "B_scale", "C_scale", "xs_scale", "state_scale",
+              "cb_scale", "corr"):
+        old = getattr(a, f)
+        setattr(a, f, None)
+        assert call(d, a) == ssdi8.ERR_NULL, f
+        setattr(a, f, old)
+    a.decay_shift = 15
+    assert call(d, a) == ssdi8.ERR_ARG
+    a.decay_shift = 7
+    a.eta = float("nan")
+    assert call(d, a) == ssdi8.ERR_ARG
+    a.eta = 0.15
+    a.workspace_bytes = ws - 1
+    assert call(d, a) == ssdi8.ERR_WORKSPACE
+    a.workspace_bytes = 1 << 40
+    a.corr = A16 + 2
+    assert call(d, a) == ssdi8.ERR_ALIGN
+    a.corr = A16
+    assert call(ssdi8.dims(0, 512, 8, 2), a) == ssdi8.ERR_SHAPE
+    assert call(ssdi8.dims(2, 300, 8, 2), a) == ssdi8.ERR_SHAPE
