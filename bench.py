@@ -24,6 +24,9 @@ HBM_PEAK_GBS = 8000.0           # MI355X HBM3E, published
 INT8_PEAK_TOPS = 5000.0         # MI355X dense int8 MFMA, published
 FP16_PEAK_TFLOPS = 2500.0       # MI355X dense fp16 MFMA, published
 MODULES = ("chunk_bmm", "chunk_state", "state_pass", "chunk_scan")
+# the single pass (fp16 x): ChunkState + StatePassing + ChunkScan in one kernel after ChunkBMM
+SINGLE = ("chunk_bmm", "single_pass")
+SOURCE = {"single_pass": "chunk_scan"}      # kernel -> source file of its HIP code
 
 
 def algorithmic_bytes(cfg):
@@ -41,6 +44,10 @@ def algorithmic_bytes(cfg):
         "chunk_state": T * H * P * sx + T * H * 4 + T * G * N + states + B * H * c * 2,
         "state_pass": 2 * states + B * H * c * 2 + B * H * P * N * 5,
         "chunk_scan": 2 * T * H * P * sx + T * H * 4 + T * G * N + states + cb_causal,
+        # x in, y out, dt, B_q^T and C_q (per group), CB_q, the entering states handed from
+        # chunk to chunk (written once, read once) and the final state (int8 + fp32)
+        "single_pass": (2 * T * H * P * sx + T * H * 4 + 2 * T * G * N + cb_causal
+                        + 2 * B * (c - 1) * H * P * N + B * H * P * N * 5),
     }
 
 
@@ -55,6 +62,8 @@ def algorithmic_ops(cfg):
         "chunk_bmm": (2 * B * c * G * pairs * N, 0),
         "chunk_state": (2 * B * c * H * Q * P * N, 0),
         "chunk_scan": (2 * B * c * H * Q * N * P, 2 * B * c * H * pairs * P),
+        "single_pass": (2 * B * c * H * Q * P * N + 2 * B * c * H * Q * N * P,
+                        2 * B * c * H * pairs * P),
     }
 
 
@@ -72,7 +81,7 @@ def measured_traffic(kernel: str, workload: str):
     there is none or the kernel's source changed since the counters were taken."""
     import hashlib
     path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload}.json")
-    src = os.path.join(ROOT, "paper_2608_21952_amd", "csrc", f"{kernel}.hip")
+    src = os.path.join(ROOT, "paper_2608_21952_amd", "csrc", f"{SOURCE.get(kernel, kernel)}.hip")
     if not os.path.exists(path) or not os.path.exists(src):
         return None
     with open(path) as f:
@@ -252,6 +261,9 @@ def main():
     ap.add_argument("--cpu-budget-s", type=float, default=15.0)
     ap.add_argument("--eager", action="store_true",
                     help="time eager launches instead of replays of one captured HIP graph")
+    ap.add_argument("--path", choices=("auto", "separate", "single"), default="auto",
+                    help="separate ChunkState / StatePassing / ChunkScan kernels, the single "
+                         "pass, or the library's automatic choice")
     ap.add_argument("--copy-probe-mb", type=int, default=0,
                     help="after the timed region, run one plain device-to-device copy of this "
                          "many MiB (a known-size reference for HBM byte counters)")
@@ -299,7 +311,7 @@ def main():
             ev.record(7 * k + 1)
         ssdi8.quantize_act(Cf, "group", aC, out=Cq)
         ssdi8.ssd_chunk_scan(x, dt, A, Bq, Cq, aB, aC, aXs, aS, aCB, D=D, corr=corr,
-                             workspace=ws, y=y, final_state=True,
+                             workspace=ws, y=y, final_state=True, path=args.path,
                              stage_events=None if k is None else ev.group(7 * k + 2))
 
     for _ in range(W):
@@ -338,14 +350,22 @@ def main():
             step(k)
         torch.cuda.synchronize()
     # per-module averages over the timed steps (events on the launch stream)
-    names = ("quantize_B", "quantize_C") + MODULES
+    single = ssdi8.uses_single_pass(ssdi8.dims(cfg.batch, cfg.seqlen, cfg.nheads, cfg.ngroups),
+                                    x.dtype, args.path)
+    mods = SINGLE if single else MODULES
+    names = ("quantize_B", "quantize_C") + mods
     per = {n: 0.0 for n in names}
     for k in range(K):
         base = 7 * k
         per["quantize_B"] += ev.elapsed_ms(base, base + 1)
         per["quantize_C"] += ev.elapsed_ms(base + 1, base + 2)
-        for i, n in enumerate(MODULES):
-            per[n] += ev.elapsed_ms(base + 2 + i, base + 3 + i)
+        if single:
+            # events 1-3 are recorded back to back before the single pass
+            per["chunk_bmm"] += ev.elapsed_ms(base + 2, base + 3)
+            per["single_pass"] += ev.elapsed_ms(base + 5, base + 6)
+        else:
+            for i, n in enumerate(MODULES):
+                per[n] += ev.elapsed_ms(base + 2 + i, base + 3 + i)
     per = {n: v / K for n, v in per.items()}
     ev.close()
     abytes = algorithmic_bytes(cfg)
@@ -356,13 +376,15 @@ def main():
     # MFMA utilisation of the contraction kernels (these shapes sit far below the machine
     # balance, so the HBM fraction is the binding one; reported for completeness)
     for n, (i8, f16) in algorithmic_ops(cfg).items():
+        if n not in per:
+            continue
         sec = per[n] * 1e-3
         stages[n]["int8_tops"] = round(i8 / sec / 1e12, 1)
         stages[n]["int8_mfma_frac"] = round(i8 / sec / 1e12 / INT8_PEAK_TOPS, 4)
         if f16:
             stages[n]["fp16_tflops"] = round(f16 / sec / 1e12, 1)
             stages[n]["fp16_mfma_frac"] = round(f16 / sec / 1e12 / FP16_PEAK_TFLOPS, 4)
-    dom = "chunk_scan"
+    dom = "single_pass" if single else "chunk_scan"
     ach = abytes[dom] / (per[dom] * 1e-3) / 1e9
     tokens = cfg.batch * cfg.seqlen
     value = tokens / (ms_step * 1e-3)
@@ -382,6 +404,8 @@ def main():
         "timing": ("K replays of one captured HIP graph; per-kernel times from K eager steps "
                    "bracketed by HIP events" if graph is not None else "eager launches"),
         "layer_hbm_frac": round(layer_min_bytes(cfg) / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "path": ("single pass: ChunkBMM, then ChunkState + StatePassing + ChunkScan in one kernel"
+                 if single else "separate ChunkBMM, ChunkState, StatePassing, ChunkScan kernels"),
         "stages": stages,
     }
     f16 = time_fp16(torch, ssdi8, cfg, x, dt, A, Bf, Cf, D, K, W)

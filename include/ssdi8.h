@@ -155,6 +155,16 @@ typedef struct {
      ChunkScan and after ChunkScan (the module breakdown of the paper's latency figures).
      Leave NULL when the call is captured into a HIP graph. */
   void* const* stage_events;
+  /* Kernel path.  With fp16 x and none of the taps xs_q, state_i32, state_q, decay_q, state_in_q,
+     scan1_i32 requested, ChunkState, StatePassing and ChunkScan can run as one single-pass
+     kernel in which each chunk waits for the previous chunk of its sequence to hand over the
+     int8 entering state (integer results identical; y differs from the separate kernels only by
+     the rounding of ChunkScan's fp32 tables).  0: automatic (the single pass when the sequences
+     have at least 16 chunks and batch * nheads >= 64, where it is the faster one: with fewer
+     chunks the per-chunk hand-off latency is not amortized, with fewer sequences their serial
+     chains bound it); 1: always the separate kernels; 2: the single pass whenever eligible.
+     With the single pass, events 1-3 of stage_events are recorded back to back before it. */
+  int path;
 } ssdi8_scan_args;
 
 /* Workspace bytes needed by ssdi8_ssd_chunk_scan for these sizes (0 on invalid sizes). */
@@ -168,6 +178,10 @@ size_t ssdi8_ssd_workspace_size(const ssdi8_dims* d);
  * already be quantized (ssdi8_quantize_act).  Intermediates go through `workspace`.
  */
 ssdi8_status ssdi8_ssd_chunk_scan(const ssdi8_dims* d, const ssdi8_scan_args* a, void* stream);
+
+/* 1 if ssdi8_ssd_chunk_scan with these arguments runs the single-pass kernel (see `path`), 0 if
+   the separate kernels (or on invalid sizes).  Host only; launches nothing. */
+int ssdi8_uses_single_pass(const ssdi8_dims* d, const ssdi8_scan_args* a);
 
 /*
  * ssdi8_decode_step — one token of every (batch, head) sequence in the recurrent mode of the same

@@ -20,7 +20,7 @@ bool aligned16_or_null(const void* p) { return p == nullptr || aligned16(p); }
 size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 struct Plan {
-  size_t bqT, cq, sq, pin, cbq, qd, total;
+  size_t bqT, cq, sq, pin, cbq, qd, sync, nsync, total;
 };
 
 // Workspace regions (256-byte aligned), the int8 ones in the MFMA fragment order of frag.hpp:
@@ -39,6 +39,9 @@ Plan plan_workspace(const ssdi8_dims* d) {
   p.cbq = off; off = round_up(off + B * nc * G * (size_t)ssdi8::frag::kCbChunkBytes, 256);
   (void)Q;
   p.qd = off;  off = round_up(off + B * H * nc * sizeof(int16_t), 256);
+  // single-pass hand-off: ticket counters, timed-out waits, one flag per (b, h, c)
+  p.nsync = ssdi8::kSyncFlags + B * H * nc;
+  p.sync = off; off = round_up(off + p.nsync * sizeof(int), 256);
   p.total = off;
   return p;
 }
@@ -116,9 +119,23 @@ ssdi8_status check_dims(const ssdi8_dims* d) {
   return SSDI8_OK;
 }
 
+// Whether ssdi8_ssd_chunk_scan runs ChunkState, StatePassing and ChunkScan as the single pass.
+bool single_pass(const ssdi8_dims* d, const ssdi8_scan_args* a) {
+  const bool eligible = a->x_dtype == SSDI8_F16 && !a->xs_q && !a->state_i32 && !a->state_q &&
+                        !a->decay_q && !a->state_in_q && !a->scan1_i32;
+  const int64_t nc = d->chunk > 0 ? d->seqlen / d->chunk : 0;
+  return eligible &&
+         (a->path == 2 || (a->path == 0 && nc >= 16 && d->batch * d->nheads >= 64));
+}
+
 }  // namespace
 
 extern "C" {
+
+int ssdi8_uses_single_pass(const ssdi8_dims* d, const ssdi8_scan_args* a) {
+  if (check_dims(d) != SSDI8_OK || !a || a->path < 0 || a->path > 2) return 0;
+  return single_pass(d, a) ? 1 : 0;
+}
 
 const char* ssdi8_version(void) { return "0.1.0"; }
 
@@ -195,6 +212,7 @@ ssdi8_status ssdi8_ssd_chunk_scan(const ssdi8_dims* d, const ssdi8_scan_args* a,
   if (a->x_dtype != SSDI8_F32 && a->x_dtype != SSDI8_F16) return SSDI8_ERR_ARG;
   if (a->y_dtype != SSDI8_F32 && a->y_dtype != SSDI8_F16) return SSDI8_ERR_ARG;
   if (a->decay_shift < 1 || a->decay_shift > 14) return SSDI8_ERR_ARG;
+  if (a->path < 0 || a->path > 2) return SSDI8_ERR_ARG;
   const bool work = d->batch > 0 && d->seqlen > 0;
   if (work && (!a->x || !a->dt || !a->A || !a->Bq || !a->Cq || !a->B_scale || !a->C_scale ||
                !a->xs_scale || !a->state_scale || !a->cb_scale || !a->y))
@@ -245,11 +263,36 @@ ssdi8_status ssdi8_ssd_chunk_scan(const ssdi8_dims* d, const ssdi8_scan_args* a,
     return !a->stage_events ||
            hipEventRecord(static_cast<hipEvent_t>(a->stage_events[i]), st) == hipSuccess;
   };
+  const bool fused = single_pass(d, a);
+  int* sync = reinterpret_cast<int*>(ws + plan.sync);
   if (!mark(0)) return SSDI8_ERR_HIP;
   hipError_t e = ssdi8::launch_chunk_bmm(ld, a->Cq, a->Bq, a->C_scale, a->c_per_token,
                                          a->B_scale, a->cb_scale, cbq, a->cb_q, a->cb_i32, bqT,
-                                         cq, st);
+                                         cq, fused ? 1 : 0, sync, fused ? (int)plan.nsync : 0,
+                                         st);
   if (e != hipSuccess || !mark(1)) return SSDI8_ERR_HIP;
+  if (fused) {
+    if (!mark(2) || !mark(3)) return SSDI8_ERR_HIP;
+    ssdi8::FusedState fs;
+    fs.bqT = bqT;
+    fs.B_scale = a->B_scale;
+    fs.xs_scale = a->xs_scale;
+    fs.xs_per_head = a->xs_per_head;
+    fs.shift = a->decay_shift;
+    fs.radd = a->shift_round ? (1 << (a->decay_shift - 1)) : 0;
+    fs.init = a->init_state_q;
+    fs.final_q = a->final_state_q;
+    fs.final_state = a->final_state;
+    fs.sync = sync;
+    fs.nbh = ld.batch * ld.nheads;
+    fs.spin_limit = 1 << 16;   // polls of ~1 us: a wait gives up after ~65 ms
+    e = ssdi8::launch_chunk_scan_fused(ld, static_cast<const _Float16*>(a->x), a->dt,
+                                       a->dt_softplus, a->A, cq, a->C_scale, a->c_per_token, pin,
+                                       cbq, a->cb_scale, a->state_scale, a->D, a->corr, a->y,
+                                       a->y_dtype, fs, st);
+    if (e != hipSuccess || !mark(4)) return SSDI8_ERR_HIP;
+    return SSDI8_OK;
+  }
   e = ssdi8::launch_chunk_state(ld, a->x, a->x_dtype, a->dt, a->dt_softplus, a->A, bqT,
                                 a->B_scale, a->xs_scale, a->xs_per_head, a->state_scale,
                                 a->decay_shift, sq, qd, a->xs_q, a->state_q, a->state_i32, st);
@@ -376,12 +419,6 @@ ssdi8_status ssdi8_calibrate(const ssdi8_dims* d, const ssdi8_calib_args* a, voi
   float* cb = reinterpret_cast<float*>(f16 + plan.f16.cb);
   float* dec = reinterpret_cast<float*>(f16 + plan.f16.dec);
   char* i8 = ws + plan.i8_base;
-  int8_t* bqT = reinterpret_cast<int8_t*>(i8 + plan.i8.bqT);
-  int8_t* cqf = reinterpret_cast<int8_t*>(i8 + plan.i8.cq);
-  int8_t* sq = reinterpret_cast<int8_t*>(i8 + plan.i8.sq);
-  int8_t* pin8 = reinterpret_cast<int8_t*>(i8 + plan.i8.pin);
-  int8_t* cbq = reinterpret_cast<int8_t*>(i8 + plan.i8.cbq);
-  int16_t* qd = reinterpret_cast<int16_t*>(i8 + plan.i8.qd);
   int8_t* Bq = reinterpret_cast<int8_t*>(ws + plan.bq);
   int8_t* Cq = reinterpret_cast<int8_t*>(ws + plan.cq);
   float* yfp = reinterpret_cast<float*>(ws + plan.yfp);
@@ -417,23 +454,33 @@ ssdi8_status ssdi8_calibrate(const ssdi8_dims* d, const ssdi8_calib_args* a, voi
   if (e == hipSuccess)
     e = ssdi8::launch_fp16_scan(ld, a->x, a->x_dtype, a->dt, a->dt_softplus, a->A, c16, pin16,
                                 cb, a->D, yfp, SSDI8_F32, st);
-  // Y_q: the INT8 layer with the new steps and no correction
-  if (e == hipSuccess)
-    e = ssdi8::launch_chunk_bmm(ld, Cq, Bq, a->C_scale, 0, a->B_scale, a->cb_scale, cbq,
-                                nullptr, nullptr, bqT, cqf, st);
-  if (e == hipSuccess)
-    e = ssdi8::launch_chunk_state(ld, a->x, a->x_dtype, a->dt, a->dt_softplus, a->A, bqT,
-                                  a->B_scale, a->xs_scale, a->xs_per_head, a->state_scale,
-                                  a->decay_shift, sq, qd, nullptr, nullptr, nullptr, st);
-  if (e == hipSuccess)
-    e = ssdi8::launch_state_pass(d->batch, ld.nchunks, d->nheads, d->headdim * d->dstate,
-                                 d->headdim, sq, qd, a->decay_shift, a->shift_round, nullptr,
-                                 pin8, nullptr, nullptr, nullptr, a->state_scale,
-                                 (int)d->dstate, st);
-  if (e == hipSuccess)
-    e = ssdi8::launch_chunk_scan(ld, a->x, a->x_dtype, a->dt, a->dt_softplus, a->A, cqf,
-                                 a->C_scale, 0, pin8, cbq, a->cb_scale, a->state_scale, a->D,
-                                 nullptr, yq, SSDI8_F32, nullptr, st);
+  // Y_q: the INT8 layer with the new steps and no correction, as ssdi8_ssd_chunk_scan runs it
+  if (e != hipSuccess) return SSDI8_ERR_HIP;
+  {
+    ssdi8_scan_args la = {};
+    la.x = a->x;
+    la.x_dtype = a->x_dtype;
+    la.dt = a->dt;
+    la.dt_softplus = a->dt_softplus;
+    la.A = a->A;
+    la.Bq = Bq;
+    la.Cq = Cq;
+    la.B_scale = a->B_scale;
+    la.C_scale = a->C_scale;
+    la.D = a->D;
+    la.xs_scale = a->xs_scale;
+    la.xs_per_head = a->xs_per_head;
+    la.state_scale = a->state_scale;
+    la.cb_scale = a->cb_scale;
+    la.decay_shift = a->decay_shift;
+    la.shift_round = a->shift_round;
+    la.y = yq;
+    la.y_dtype = SSDI8_F32;
+    la.workspace = i8;
+    la.workspace_bytes = plan.i8.total;
+    const ssdi8_status ls = ssdi8_ssd_chunk_scan(d, &la, stream);
+    if (ls != SSDI8_OK) return ls;
+  }
   if (e == hipSuccess)
     e = ssdi8::launch_calib_corr(yfp, yq, a->corr, d->batch * d->seqlen, H, a->eta, st);
   return e == hipSuccess ? SSDI8_OK : SSDI8_ERR_HIP;

@@ -32,10 +32,13 @@ __global__ __launch_bounds__(256) void chunk_bmm_kernel(
     const float* __restrict__ C_scale, int c_per_token, const float* __restrict__ B_scale,
     const float* __restrict__ cb_scale, int8_t* __restrict__ cbq_frag,
     int8_t* __restrict__ cbq_tap, int32_t* __restrict__ cb32_tap, int8_t* __restrict__ bqT_frag,
-    int8_t* __restrict__ cq_frag, int L, int G, int nc) {
+    int8_t* __restrict__ cq_frag, int cq_perm, int* __restrict__ sync, int nsync, int L, int G,
+    int nc) {
   __shared__ __attribute__((aligned(16))) int8_t s_b[kQ * kBS];
 
   const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
+  // clears the ticket and hand-off flags of the single-pass scan that follows in the stream
+  for (int i = blockIdx.x * 256 + t; i < nsync; i += gridDim.x * 256) sync[i] = 0;
   const int w = xcd_remap(blockIdx.x, gridDim.x);
   const int role = w % kRoles;
   const int bcg = w / kRoles;
@@ -113,10 +116,24 @@ __global__ __launch_bounds__(256) void chunk_bmm_kernel(
     // the C_q rows of block jt, in ChunkScan1 fragment order (before the MFMA chain, so that no
     // branch separates the last MFMA from the reads of its result)
     int8_t* cdst = cq_frag + cg * (size_t)kQ * kN;
+    if (cq_perm) {
+      // permuted kslice order: lane (j, h) takes n = 8 g + 4 h + i; it holds n = 16 h + [0, 16)
+      // and swaps the other half-wave's two runs of 4 with lane l ^ 32
+      const int hl = lane >> 5;
 #pragma unroll
-    for (int ks = 0; ks < kN / 32; ++ks)
-      *reinterpret_cast<v4i*>(cdst + frag::kslice_offset(jt * 32 + (lane & 31),
-                                                         32 * ks + 16 * (lane >> 5), kN)) = a[ks];
+      for (int ks = 0; ks < kN / 32; ++ks) {
+        const int s0 = hl ? a[ks][0] : a[ks][1], s1 = hl ? a[ks][2] : a[ks][3];
+        const int r0 = __shfl_xor(s0, 32, 64), r1 = __shfl_xor(s1, 32, 64);
+        const v4i o = hl ? v4i{r0, r1, a[ks][1], a[ks][3]} : v4i{a[ks][0], a[ks][2], r0, r1};
+        *reinterpret_cast<v4i*>(cdst + ((size_t)jt * (kN / 32) + ks) * 1024 + lane * 16) = o;
+      }
+    } else {
+#pragma unroll
+      for (int ks = 0; ks < kN / 32; ++ks)
+        *reinterpret_cast<v4i*>(cdst + frag::kslice_offset(jt * 32 + (lane & 31),
+                                                           32 * ks + 16 * (lane >> 5), kN)) =
+            a[ks];
+    }
   }
   v16i acc = {};
 #pragma unroll
@@ -154,13 +171,13 @@ __global__ __launch_bounds__(256) void chunk_bmm_kernel(
 hipError_t launch_chunk_bmm(const LayerDims& d, const int8_t* Cq, const int8_t* Bq,
                             const float* C_scale, int c_per_token, const float* B_scale,
                             const float* cb_scale, int8_t* cbq_frag, int8_t* cbq_tap,
-                            int32_t* cb32_tap, int8_t* bqT_frag, int8_t* cq_frag,
-                            hipStream_t st) {
+                            int32_t* cb32_tap, int8_t* bqT_frag, int8_t* cq_frag, int cq_perm,
+                            int* sync, int nsync, hipStream_t st) {
   const int64_t nwork = (int64_t)d.batch * d.nchunks * d.ngroups * kRoles;
   if (nwork == 0) return hipSuccess;
   hipLaunchKernelGGL(chunk_bmm_kernel, dim3((unsigned)nwork), dim3(256), 0, st, Cq, Bq, C_scale,
                      c_per_token, B_scale, cb_scale, cbq_frag, cbq_tap, cb32_tap, bqT_frag,
-                     cq_frag, d.seqlen, d.ngroups, d.nchunks);
+                     cq_frag, cq_perm, sync, nsync, d.seqlen, d.ngroups, d.nchunks);
   return hipGetLastError();
 }
 

@@ -71,21 +71,31 @@ __device__ __forceinline__ float softplus_fast(float v) {
   return v > 20.0f ? v : lp;
 }
 
-template <typename XT, typename YT>
+// One INT8 StatePassing step of an element (Eq. 9): clamp(S_q + ((q_d P_in + r) >> k)).
+__device__ __forceinline__ int pass_step(int s, int add, int q, int shift, int radd) {
+  const int v = add + ((q * s + radd) >> shift);
+  return v < -kQMax ? -kQMax : (v > kQMax ? kQMax : v);
+}
+
+template <typename XT, typename YT, bool kFused>
 __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
     const XT* __restrict__ x, const float* __restrict__ dt, const float* __restrict__ A,
     const int8_t* __restrict__ cq_frag, const float* __restrict__ C_scale, int c_per_token,
-    const int8_t* __restrict__ pin, const int8_t* __restrict__ cbq,
+    int8_t* __restrict__ pin, const int8_t* __restrict__ cbq,
     const float* __restrict__ cb_scale, const float* __restrict__ state_scale,
     const float* __restrict__ Dv, const float* __restrict__ corr, int dt_softplus,
-    YT* __restrict__ y, int32_t* __restrict__ y1_tap, int L, int H, int G, int nc) {
+    YT* __restrict__ y, int32_t* __restrict__ y1_tap, int L, int H, int G, int nc,
+    FusedState fs) {
   // One LDS block with the small per-token tables first, so that their offsets fit the 16-bit
   // ds offset field (separate __shared__ arrays may be placed large-first).
   struct __attribute__((aligned(16))) Smem {
     // Column tables of the ChunkScan2 weights, interleaved as (w, -128 w) pairs so that an int8
     // weight q, converted as the unsigned byte q + 128, gives fl32(q w) = fma(q + 128, w, -128 w)
     // exactly (the fma forms (q + 128) w - 128 w = q w before its one rounding).
-    float2 u[kQ];        // a_CB dt_i exp(r_I - cs_i)                  (off-diagonal blocks)
+    union {
+      float2 u[kQ];      // a_CB dt_i exp(r_I - cs_i)                  (off-diagonal blocks)
+      float lut[kQ];     // single pass: LUT_state of ChunkState, read before u is built
+    };
     float2 dg[kQ];       // a_CB dt_i exp(r_{I-1} - cs_i) if block I has a small span, else
                          // a_CB dt_i                                   (diagonal blocks)
     float csr[kQ];       // cs_i - r_{I-1} (r_{-1} = 0), fp32
@@ -94,6 +104,7 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
     float cr[kP];
     double r[8];         // r_t: cs at the last token of block t
     double scan[4];
+    int misc[4];         // single pass: ticket, q_d
     // x^T [p][i] fp16: the ChunkScan2 MFMA operand and, for fp16 x, the D skip operand; then
     // the stage of the fp16 output (256 rows of 128 bytes).
     uint8_t xT[kP * kXTS];
@@ -111,11 +122,44 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
 
   const int t = threadIdx.x, lane = t & 63;
   const int wv = __builtin_amdgcn_readfirstlane(t >> 6);   // wave-uniform, so block loops are scalar
-  const int w = xcd_remap(blockIdx.x, gridDim.x);
-  const int h = w % H;
-  const int bc = w / H;
-  const int c = bc % nc;
-  const int b = bc / nc;
+  int b, c, h;
+  if constexpr (kFused) {
+    // Work items in ticket order.  The sequences (b, h) are dealt to 8 classes (bh % 8); class x
+    // hands out its items chunk-major from its own counter sync[x], so the item a workgroup
+    // waits for (same sequence, previous chunk) holds an earlier ticket of the same counter and
+    // is running or done.  A workgroup draws from class blockIdx % 8 (with round-robin dispatch
+    // over the 8 XCDs, a sequence stays on one XCD) and, once that class is exhausted, from the
+    // next ones; the grid has as many workgroups as items, so every item is drawn.
+    if (t == 0) {
+      const int nbh = fs.nbh;
+      int item = -1;
+      for (int k = 0; k < kSyncClasses && item < 0; ++k) {
+        const int x = (int)((blockIdx.x + k) & (kSyncClasses - 1));
+        const int chains = (nbh - x + kSyncClasses - 1) / kSyncClasses;
+        if (chains <= 0) continue;
+        const int tk = atomicAdd(fs.sync + x, 1);
+        if (tk < chains * nc) {
+          const int cc = tk / chains;
+          item = cc * nbh + x + kSyncClasses * (tk - cc * chains);
+        }
+      }
+      sm.misc[0] = item;
+    }
+    __syncthreads();
+    const int item = __builtin_amdgcn_readfirstlane(sm.misc[0]);
+    if (item < 0) return;   // every item drawn (only with an uncleared counter)
+    const int nbh = fs.nbh;
+    c = item / nbh;
+    const int bh = item - c * nbh;
+    b = bh / H;
+    h = bh - b * H;
+  } else {
+    const int w = xcd_remap(blockIdx.x, gridDim.x);
+    h = w % H;
+    const int bc = w / H;
+    c = bc % nc;
+    b = bc / nc;
+  }
   const int g = h / (H / G);
   const size_t tok0 = (size_t)b * L + (size_t)c * kQ;
   const size_t HP = (size_t)H * kP;
@@ -133,7 +177,8 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
 
   // ---- ChunkCumsum (fp64 sums; the factors derived from it only need fp32 accuracy here)
   float dtv = dt[(tok0 + t) * H + h];
-  if (dt_softplus) dtv = softplus_fast(dtv);
+  // the single pass quantizes X_scaled, which needs the fp64 softplus of ChunkState
+  if (dt_softplus) dtv = kFused ? softplus_f32(dtv) : softplus_fast(dtv);
   const float dA = dtv * A[h];
   const double cs = block_scan_f64_256((double)dA, s_scan);
   if ((t & 31) == 31) s_r[t >> 5] = cs;
@@ -142,7 +187,8 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
     s_cr[t] = corr ? corr[h * kP + t] : 0.0f;
   }
   __syncthreads();
-  {
+  // ChunkScan2's tables (the single pass builds them after ChunkState: u shares LDS with LUT)
+  auto scan_tables = [&]() {
     const int blk = t >> 5;
     const double rprev = blk ? s_r[blk - 1] : 0.0;
     const float dtcb = aCB * dtv;
@@ -158,6 +204,13 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
       const int ra = t >> 3, rb = t & 7;
       s_R[ra][rb] = (rb <= ra) ? expf((float)(s_r[ra] - s_r[rb])) : 0.0f;
     }
+  };
+  if constexpr (!kFused) scan_tables();
+  if constexpr (kFused) {
+    // ChunkState's table and Q(Decay), with its exact arithmetic (Eq. 4, Eq. 9)
+    const double last = s_r[7];
+    sm.lut[t] = dtv * (float)exp(last - cs);
+    if (t == 0) sm.misc[1] = (int)rint(exp(last) * (double)(1 << fs.shift));
   }
   // ---- x^T [p][i] (fp16) in LDS
   {
@@ -177,6 +230,143 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
     }
   }
   __syncthreads();
+
+  // single pass: wave -> channel tile mt and state tiles ntb, ntb + 1; lane -> channel prow
+  const int hf = lane >> 5, mt = wv & 1, ntb = (wv >> 1) * 2;
+  const int prow = mt * 32 + (lane & 31);
+  uint32_t sq[2][4];   // S_q of the two tiles, byte r of word r / 4 = MFMA result row r
+  if constexpr (kFused) {
+    // ---- ChunkState (Eq. 7-8), transposed: S32^T = B_q^T X_q with X_q formed from the x^T
+    //      bytes in LDS.  Lane -> channel p = 32 mt + l % 32 and, per tile, the 16 state rows n
+    //      of the permuted kslice order (frag.hpp), which is where the MFMA leaves them.
+    const float axs = fs.xs_per_head ? fs.xs_scale[h] : fs.xs_scale[h * kP + prow];
+    const float inv = 1.0f / axs;
+    const float msp =
+        (float)(((double)axs * (double)fs.B_scale[g]) / (double)state_scale[h * kP + prow]);
+    {
+      const __amdgpu_buffer_rsrc_t brs =
+          buffer_rsrc(fs.bqT + (((size_t)b * nc + c) * G + g) * (size_t)kN * kQ);
+      const uint32_t l16 = lane * 16;
+      v16i s0 = {}, s1 = {};
+#pragma unroll
+      for (int ks = 0; ks < kQ / 32; ++ks) {
+        const v4i bf0 = __builtin_bit_cast(
+            v4i, buf_load16(brs, l16, (uint32_t)((ntb * (kQ / 32) + ks) * 1024)));
+        const v4i bf1 = __builtin_bit_cast(
+            v4i, buf_load16(brs, l16, (uint32_t)(((ntb + 1) * (kQ / 32) + ks) * 1024)));
+        const int j0 = ks * 32 + 16 * hf;
+        const uint4 xa = *reinterpret_cast<const uint4*>(s_xT + prow * kXTS + j0 * 2);
+        const uint4 xb = *reinterpret_cast<const uint4*>(s_xT + prow * kXTS + j0 * 2 + 16);
+        const uint32_t xw[8] = {xa.x, xa.y, xa.z, xa.w, xb.x, xb.y, xb.z, xb.w};
+        uint32_t qw[4];
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+          const float4 l4 = *reinterpret_cast<const float4*>(sm.lut + j0 + 4 * q4);
+          const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
+          int qv[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const uint32_t wd = xw[2 * q4 + (e >> 1)];
+            const float xv = (float)__builtin_bit_cast(
+                _Float16, (uint16_t)((e & 1) ? (wd >> 16) : (wd & 0xffffu)));
+            qv[e] = quant_i8(lv[e] * xv, inv);
+          }
+          qw[q4] = pack4_i8(qv[0], qv[1], qv[2], qv[3]);
+        }
+        const v4i a = {(int)qw[0], (int)qw[1], (int)qw[2], (int)qw[3]};
+        s0 = __builtin_amdgcn_mfma_i32_32x32x32_i8(bf0, a, s0, 0, 0, 0);
+        s1 = __builtin_amdgcn_mfma_i32_32x32x32_i8(bf1, a, s1, 0, 0, 0);
+      }
+      // S_q = requant(S32, m_S[p]) (Eq. 8), one multiplier per lane
+#pragma unroll
+      for (int w4 = 0; w4 < 4; ++w4) {
+        sq[0][w4] = pack4_i8(requant_i8(s0[4 * w4], msp), requant_i8(s0[4 * w4 + 1], msp),
+                             requant_i8(s0[4 * w4 + 2], msp), requant_i8(s0[4 * w4 + 3], msp));
+        sq[1][w4] = pack4_i8(requant_i8(s1[4 * w4], msp), requant_i8(s1[4 * w4 + 1], msp),
+                             requant_i8(s1[4 * w4 + 2], msp), requant_i8(s1[4 * w4 + 3], msp));
+      }
+    }
+    __syncthreads();   // LUT no longer read: its bytes become ChunkScan2's u table
+    scan_tables();
+    __syncthreads();
+  }
+
+  // ---- single pass, StatePassing (Eq. 9) for this chunk: wait until the previous chunk of the
+  //      sequence has published P_in[c] (bounded: a wait
+  //      that runs out is counted in sync[8] and the kernel still finishes), then
+  //      P_in[c+1] = clamp(S_q + ((q_d P_in[c] + r) >> k)), published with agent-coherent
+  //      stores before the flag.  Every lane updates its own 32 state bytes in registers.
+  auto hand_off = [&]() {
+    const int bh = b * H + h;
+    int* flags = fs.sync + kSyncFlags;
+    if (c > 0 && t == 0) {
+      const int* f = flags + (size_t)bh * nc + (c - 1);
+      int ok = 0;
+      for (int it = 0; it < fs.spin_limit; ++it) {
+        if (__hip_atomic_load(f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) {
+          ok = 1;
+          break;
+        }
+        __builtin_amdgcn_s_sleep(2);
+      }
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+      if (!ok) atomicAdd(fs.sync + kSyncClasses, 1);
+    }
+    __syncthreads();
+    {
+      constexpr size_t kSlab = (size_t)kP * kN;
+      const int qd = sm.misc[1];
+      int8_t* slab = pin + (((size_t)b * nc + c) * H + h) * kSlab;
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const uint32_t off = (uint32_t)((mt * (kN / 32) + ntb + i) * 1024 + lane * 16);
+        // row-major (p, n) of this lane's byte 4 g + e: p = prow, n = 32 (ntb + i) + 8 g + 4 hf + e
+        const size_t rbase = (size_t)bh * kSlab + (size_t)prow * kN + 32 * (ntb + i) + 4 * hf;
+        uint32_t cw[4];
+        if (c > 0) {
+          const uint4 v = *reinterpret_cast<const uint4*>(slab + off);
+          cw[0] = v.x; cw[1] = v.y; cw[2] = v.z; cw[3] = v.w;
+        } else {
+#pragma unroll
+          for (int g4 = 0; g4 < 4; ++g4)
+            cw[g4] = fs.init ? *reinterpret_cast<const uint32_t*>(fs.init + rbase + 8 * g4) : 0u;
+          // the entering state of the first chunk, in the order ChunkScan1 reads it
+          *reinterpret_cast<uint4*>(slab + off) = make_uint4(cw[0], cw[1], cw[2], cw[3]);
+        }
+        uint32_t nw[4];
+#pragma unroll
+        for (int g4 = 0; g4 < 4; ++g4) {
+          int v[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            v[e] = pass_step(sext8(cw[g4], e), sext8(sq[i][g4], e), qd, fs.shift, fs.radd);
+          nw[g4] = pack4_i8(v[0], v[1], v[2], v[3]);
+        }
+        if (c + 1 < nc) {
+          typedef uint32_t u32x4 __attribute__((vector_size(16)));
+          const u32x4 v = {nw[0], nw[1], nw[2], nw[3]};
+          // sc1: written through to the agent's coherence point
+          __builtin_amdgcn_raw_buffer_store_b128(v, buffer_rsrc(slab + kSlab * H), (int)off, 0,
+                                                 16);
+        } else {
+          const float a = state_scale[h * kP + prow];
+#pragma unroll
+          for (int g4 = 0; g4 < 4; ++g4) {
+            if (fs.final_q) *reinterpret_cast<uint32_t*>(fs.final_q + rbase + 8 * g4) = nw[g4];
+            if (fs.final_state)
+              *reinterpret_cast<float4*>(fs.final_state + rbase + 8 * g4) =
+                  make_float4((float)sext8(nw[g4], 0) * a, (float)sext8(nw[g4], 1) * a,
+                              (float)sext8(nw[g4], 2) * a, (float)sext8(nw[g4], 3) * a);
+          }
+        }
+      }
+      __builtin_amdgcn_s_waitcnt(0);
+    }
+    __syncthreads();
+    if (t == 0 && c + 1 < nc)
+      __hip_atomic_store(flags + (size_t)bh * nc + c, 1, __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+  };
 
   // Both products are formed transposed (MFMA rows = channels p, columns = tokens j), so each
   // lane owns one token row j and runs of 4 consecutive channels: the epilogue needs one row
@@ -375,6 +565,7 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
       }
     }
   };
+  if constexpr (kFused) hand_off();
   jblock(wv, y_first);
   jblock(7 - wv, y_second);
 
@@ -424,16 +615,38 @@ hipError_t launch_chunk_scan(const LayerDims& d, const void* x, int x_dtype, con
   if (nwork == 0) return hipSuccess;
   const dim3 grid((unsigned)nwork), block(256);
 #define SSDI8_SCAN_LAUNCH(XT, YT)                                                             \
-  hipLaunchKernelGGL((chunk_scan_kernel<XT, YT>), grid, block, 0, st,                         \
-                     static_cast<const XT*>(x), dt, A, cq_frag, C_scale, c_per_token, pin,    \
-                     cbq, cb_scale, state_scale, D, corr, dt_softplus, static_cast<YT*>(y),   \
-                     y1_tap,                                                                  \
-                     d.seqlen, d.nheads, d.ngroups, d.nchunks)
+  hipLaunchKernelGGL((chunk_scan_kernel<XT, YT, false>), grid, block, 0, st,                  \
+                     static_cast<const XT*>(x), dt, A, cq_frag, C_scale, c_per_token,         \
+                     const_cast<int8_t*>(pin), cbq, cb_scale, state_scale, D, corr,           \
+                     dt_softplus, static_cast<YT*>(y), y1_tap, d.seqlen, d.nheads, d.ngroups, \
+                     d.nchunks, FusedState{})
   if (x_dtype == 1 && y_dtype == 1) SSDI8_SCAN_LAUNCH(_Float16, _Float16);
   else if (x_dtype == 1) SSDI8_SCAN_LAUNCH(_Float16, float);
   else if (y_dtype == 1) SSDI8_SCAN_LAUNCH(float, _Float16);
   else SSDI8_SCAN_LAUNCH(float, float);
 #undef SSDI8_SCAN_LAUNCH
+  return hipGetLastError();
+}
+
+hipError_t launch_chunk_scan_fused(const LayerDims& d, const _Float16* x, const float* dt,
+                                   int dt_softplus, const float* A, const int8_t* cq_frag,
+                                   const float* C_scale, int c_per_token, int8_t* pin,
+                                   const int8_t* cbq, const float* cb_scale,
+                                   const float* state_scale, const float* D, const float* corr,
+                                   void* y, int y_dtype, const FusedState& fs, hipStream_t st) {
+  const int64_t nwork = (int64_t)d.batch * d.nchunks * d.nheads;
+  if (nwork == 0) return hipSuccess;
+  const dim3 grid((unsigned)nwork), block(256);
+  if (y_dtype == 1)
+    hipLaunchKernelGGL((chunk_scan_kernel<_Float16, _Float16, true>), grid, block, 0, st, x, dt,
+                       A, cq_frag, C_scale, c_per_token, pin, cbq, cb_scale, state_scale, D,
+                       corr, dt_softplus, static_cast<_Float16*>(y), nullptr, d.seqlen,
+                       d.nheads, d.ngroups, d.nchunks, fs);
+  else
+    hipLaunchKernelGGL((chunk_scan_kernel<_Float16, float, true>), grid, block, 0, st, x, dt, A,
+                       cq_frag, C_scale, c_per_token, pin, cbq, cb_scale, state_scale, D, corr,
+                       dt_softplus, static_cast<float*>(y), nullptr, d.seqlen, d.nheads,
+                       d.ngroups, d.nchunks, fs);
   return hipGetLastError();
 }
 

@@ -6,6 +6,13 @@
 // 16-byte slices are consecutive, a wave fetches a whole fragment as one contiguous 1 KB run
 // instead of 32 partial rows.
 //   kslice order: tile (row / 32, k / 32) at ((row / 32) (K / 32) + k / 32) * 1 KB.
+//   permuted kslice order (pk): the same tiles and lane slices, with the K values of a 32-wide
+//                 block dealt to the two half-waves in runs of 4: lane l holds, at byte
+//                 4 g + i, k = 8 g + 4 (l / 32) + i (g, i < 4).  A contraction is unchanged
+//                 when both operands permute K alike, and this is exactly the row order in
+//                 which a 32x32 MFMA result leaves its lanes: lane l holds column l % 32 at
+//                 rows 8 (r / 4) + 4 (l / 32) + r % 4.  The single-pass scan keeps its chunk
+//                 states in this order in registers and hands them on without a transpose.
 //   CB order:     the 36 causal 32x32 blocks (J, I <= J) of a 256x256 chunk; lane l of block
 //                 (J, I) holds row j = 32 J + l % 32 and the bytes i = 32 I + 16 ks + 8 (l / 32)
 //                 + e (ks = 0, 1; e < 8) in the order [ks][e]: the two K-slices of the fp16
@@ -27,6 +34,24 @@ constexpr int kCbChunkBytes = kCbBlocks * 1024;
 __host__ __device__ __forceinline__ size_t kslice_offset(int row, int k, int K) {
   const int lane = (row & 31) + 32 * ((k & 31) >> 4);
   return ((size_t)(row >> 5) * (K >> 5) + (k >> 5)) * 1024 + lane * 16 + (k & 15);
+}
+
+// Byte offset of element (row, k) in permuted kslice order (see above).
+__host__ __device__ __forceinline__ size_t pk_offset(int row, int k, int K) {
+  const int kk = k & 31;
+  const int lane = (row & 31) + 32 * ((kk >> 2) & 1);
+  const int q = 4 * (kk >> 3) + (kk & 3);
+  return ((size_t)(row >> 5) * (K >> 5) + (k >> 5)) * 1024 + lane * 16 + q;
+}
+
+// Inverse of pk_offset.
+__host__ __device__ __forceinline__ void pk_coords(size_t off, int K, int* row, int* k) {
+  const size_t blk = off >> 10;
+  const int kb = K >> 5;
+  const int lane = (int)((off >> 4) & 63);
+  const int q = (int)(off & 15);
+  *row = (int)(blk / kb) * 32 + (lane & 31);
+  *k = (int)(blk % kb) * 32 + 8 * (q >> 2) + 4 * (lane >> 5) + (q & 3);
 }
 
 // Inverse of kslice_offset: the (row, k) of byte offset `off`.

@@ -21,12 +21,14 @@ hipError_t launch_quantize(const void* src, int src_dtype, int64_t b, int64_t l,
 // ChunkBMM (int8 C.B^T per chunk and group, causal, requantized) plus the operand copies the
 // later kernels read, all in the fragment order of frag.hpp: CB_q (36 KB per chunk and group),
 // B_q^T of the chunk ([n][j] as kslice order, ChunkState) and C_q of the chunk ([j][n] as
-// kslice order, ChunkScan1).  The taps are row-major [j][i].
+// kslice order, ChunkScan1; permuted kslice order with cq_perm, for the single pass).  The taps
+// are row-major [j][i].  sync[0, nsync) is cleared (the ticket and flags of
+// launch_chunk_scan_fused; nsync = 0 when that kernel does not follow).
 hipError_t launch_chunk_bmm(const LayerDims& d, const int8_t* Cq, const int8_t* Bq,
                             const float* C_scale, int c_per_token, const float* B_scale,
                             const float* cb_scale, int8_t* cbq_frag, int8_t* cbq_tap,
-                            int32_t* cb32_tap, int8_t* bqT_frag, int8_t* cq_frag,
-                            hipStream_t st);
+                            int32_t* cb32_tap, int8_t* bqT_frag, int8_t* cq_frag, int cq_perm,
+                            int* sync, int nsync, hipStream_t st);
 
 // ChunkCumsum + reformulated ChunkState (Eq. 7-8) and Q(Decay) (Eq. 9).
 hipError_t launch_chunk_state(const LayerDims& d, const void* x, int x_dtype, const float* dt,
@@ -51,6 +53,35 @@ hipError_t launch_chunk_scan(const LayerDims& d, const void* x, int x_dtype, con
                              const int8_t* cbq, const float* cb_scale, const float* state_scale,
                              const float* D, const float* corr, void* y, int y_dtype,
                              int32_t* y1_tap, hipStream_t st);
+
+// Single pass of ChunkState, StatePassing and ChunkScan (fp16 x): one workgroup per (b, c, h)
+// in ticket order; each computes its chunk's S_q, waits for the previous chunk of its sequence
+// to publish P_in[c] (pin slot c, permuted kslice order, as C_q), publishes P_in[c+1] (slot
+// c + 1, or the final states) and runs ChunkScan1/2 with x still in LDS.  sync: [0, 8) the
+// ticket counters of the 8 sequence classes, [8] count of waits that ran out,
+// [16 + (b H + h) nc + c] flag "slot c + 1 published"; cleared beforehand (ChunkBMM).
+constexpr int kSyncClasses = 8;
+constexpr int kSyncFlags = 16;
+struct FusedState {
+  const int8_t* bqT = nullptr;
+  const float* B_scale = nullptr;
+  const float* xs_scale = nullptr;
+  int xs_per_head = 0;
+  int shift = 7;
+  int radd = 0;
+  const int8_t* init = nullptr;
+  int8_t* final_q = nullptr;
+  float* final_state = nullptr;
+  int* sync = nullptr;
+  int nbh = 0;
+  int spin_limit = 0;
+};
+hipError_t launch_chunk_scan_fused(const LayerDims& d, const _Float16* x, const float* dt,
+                                   int dt_softplus, const float* A, const int8_t* cq_frag,
+                                   const float* C_scale, int c_per_token, int8_t* pin,
+                                   const int8_t* cbq, const float* cb_scale,
+                                   const float* state_scale, const float* D, const float* corr,
+                                   void* y, int y_dtype, const FusedState& fs, hipStream_t st);
 
 // One-token decode step on the persistent int8 state (a chunk of one token), in place.
 hipError_t launch_decode(int64_t batch, int64_t nheads, int64_t ngroups, const void* x,

@@ -47,7 +47,7 @@ class ScanArgs(ctypes.Structure):
         ("xs_q", _P), ("state_i32", _P), ("state_q", _P), ("decay_q", _P), ("state_in_q", _P),
         ("cb_i32", _P), ("cb_q", _P), ("scan1_i32", _P),
         ("workspace", _P), ("workspace_bytes", ctypes.c_size_t),
-        ("stage_events", _P),
+        ("stage_events", _P), ("path", _I),
     ]
 
 
@@ -68,6 +68,9 @@ class Fp16Args(ctypes.Structure):
         ("y", _P), ("y_dtype", _I), ("final_state", _P),
         ("workspace", _P), ("workspace_bytes", ctypes.c_size_t), ("stage_events", _P),
     ]
+
+
+PATHS = {"auto": 0, "separate": 1, "single": 2}
 
 
 class CalibArgs(ctypes.Structure):
@@ -103,6 +106,8 @@ def lib() -> ctypes.CDLL:
     L.ssdi8_ssd_workspace_size.restype = ctypes.c_size_t
     L.ssdi8_ssd_chunk_scan.argtypes = [ctypes.POINTER(Dims), ctypes.POINTER(ScanArgs), _P]
     L.ssdi8_ssd_chunk_scan.restype = _I
+    L.ssdi8_uses_single_pass.argtypes = [ctypes.POINTER(Dims), ctypes.POINTER(ScanArgs)]
+    L.ssdi8_uses_single_pass.restype = _I
     L.ssdi8_decode_step.argtypes = [i64, i64, i64, i64, i64, ctypes.POINTER(DecodeArgs), _P]
     L.ssdi8_decode_step.restype = _I
     L.ssdi8_fp16_workspace_size.argtypes = [ctypes.POINTER(Dims)]
@@ -249,12 +254,14 @@ def ssd_chunk_scan(x: torch.Tensor, dt: torch.Tensor, A: torch.Tensor, Bq: torch
                    y_dtype: Optional[torch.dtype] = None, final_state: bool = True,
                    taps: Iterable[str] = (), workspace: Optional[torch.Tensor] = None,
                    y: Optional[torch.Tensor] = None, stage_events=None,
-                   stream=None) -> Dict[str, torch.Tensor]:
+                   path: str = "auto", stream=None) -> Dict[str, torch.Tensor]:
     """One SSDi8 SSD layer (ssdi8_ssd_chunk_scan).  Shapes: x (B,L,H,P), dt (B,L,H), A (H),
     Bq/Cq (B,L,G,N) int8, B_scale (G), C_scale (G) or (B,L,G) for per-token C steps,
     xs_scale (H,P) or (H), state_scale (H,P), cb_scale (G), D (H), corr (H,P).
     Returns y, final_state_q, final_state and the requested taps (zero-initialised tensors,
-    so entries a stage does not write, such as C.B^T above the diagonal, read as 0)."""
+    so entries a stage does not write, such as C.B^T above the diagonal, read as 0).
+    path: "auto", "separate" (ChunkState, StatePassing, ChunkScan kernels) or "single" (the
+    single-pass kernel whenever x is fp16 and no stage tap is requested)."""
     _need(x, "x")
     B, L, H, P = x.shape
     _need(Bq, "Bq", torch.int8)
@@ -312,6 +319,7 @@ def ssd_chunk_scan(x: torch.Tensor, dt: torch.Tensor, A: torch.Tensor, Bq: torch
     a.workspace, a.workspace_bytes = _ptr(workspace), workspace.numel()
     if stage_events is not None:
         a.stage_events = ctypes.cast(stage_events, ctypes.c_void_p)
+    a.path = PATHS[path]
     st = lib().ssdi8_ssd_chunk_scan(ctypes.byref(d), ctypes.byref(a), _stream(stream))
     _check(st, "ssdi8_ssd_chunk_scan")
     return out
@@ -365,6 +373,16 @@ def ssd_chunk_scan_fp16(x: torch.Tensor, dt: torch.Tensor, A: torch.Tensor, B: t
     st = lib().ssdi8_ssd_chunk_scan_fp16(ctypes.byref(d), ctypes.byref(a), _stream(stream))
     _check(st, "ssdi8_ssd_chunk_scan_fp16")
     return out
+
+
+def uses_single_pass(d: Dims, x_dtype: torch.dtype, path: str = "auto", taps=()) -> bool:
+    """Whether ssd_chunk_scan on these sizes runs the single-pass kernel (ssdi8_uses_single_pass)."""
+    a = ScanArgs()
+    a.x_dtype = F16 if x_dtype == torch.float16 else F32
+    a.path = PATHS[path]
+    for name in taps:
+        setattr(a, name, 16)      # a non-NULL tap pointer (only its presence matters here)
+    return bool(lib().ssdi8_uses_single_pass(ctypes.byref(d), ctypes.byref(a)))
 
 
 def fp16_workspace_size(d: Dims) -> int:
@@ -489,7 +507,7 @@ class SSDi8Layer:
         self.Bq = self.Cq = None
 
     def __call__(self, x, dt, B, C, *, y=None, taps=(), final_state=True, stage_events=None,
-                 stream=None):
+                 path="auto", stream=None):
         Bt, L, H, P = x.shape
         G = B.shape[2]
         if self.Bq is None or self.Bq.shape != B.shape:
@@ -506,7 +524,7 @@ class SSDi8Layer:
                               decay_shift=self.decay_shift, shift_round=self.shift_round,
                               taps=taps, workspace=self.workspace, y=y,
                               final_state=final_state, stage_events=stage_events,
-                              stream=stream)
+                              path=path, stream=stream)
 
 
 # ------------------------------------------------------------------------------ timing events

@@ -174,9 +174,10 @@ def test_workspace_size(ssdi8):
     B, L, H, P, G, N, Q = 4, 4096, 80, 64, 1, 128, 256
     c = L // Q
     # B_q^T and C_q copies, S_q and P_in, the 36 causal 32x32 blocks of CB_q, Q(Decay)
-    need = 2 * B * L * G * N + 2 * B * c * H * P * N + B * c * G * 36 * 32 * 32 + B * H * c * 2
+    need = (2 * B * L * G * N + 2 * B * c * H * P * N + B * c * G * 36 * 32 * 32 + B * H * c * 2
+            + 4 * (16 + B * H * c))     # + the single-pass ticket counters, wait counter, flags
     ws = ssdi8.workspace_size(d)
-    assert need <= ws <= need + 6 * 256
+    assert need <= ws <= need + 7 * 256
     assert ssdi8.workspace_size(ssdi8.dims(1, 300, 4, 1)) == 0          # L % chunk
     assert ssdi8.workspace_size(ssdi8.dims(1, 512, 6, 4)) == 0          # H % G
     assert ssdi8.workspace_size(ssdi8.dims(1, 512, 4, 1, headdim=32)) == 0
@@ -327,3 +328,34 @@ def test_calib_argument_errors_and_workspace(ssdi8):
     a.corr = A16
     assert call(ssdi8.dims(0, 512, 8, 2), a) == ssdi8.ERR_SHAPE
     assert call(ssdi8.dims(2, 300, 8, 2), a) == ssdi8.ERR_SHAPE
+
+
+def test_single_pass_selection(ssdi8):
+    """The automatic choice between the single pass and the separate kernels (host only)."""
+    import torch
+    f16, f32 = torch.float16, torch.float32
+    use = lambda dd, *a, **k: ssdi8.uses_single_pass(dd, *a, **k)
+    assert not use(ssdi8.dims(8, 2048, 24, 1), f16)            # 8 chunks: separate
+    assert use(ssdi8.dims(4, 4096, 80, 1), f16)                # 16 chunks, 320 sequences
+    assert use(ssdi8.dims(2, 8192, 128, 8), f16)
+    assert use(ssdi8.dims(1, 65536, 80, 1), f16)               # 80 sequences of 256 chunks
+    assert not use(ssdi8.dims(1, 65536, 48, 1), f16)           # 48 sequences: chain-bound
+    assert use(ssdi8.dims(8, 2048, 24, 1), f16, "single")
+    assert not use(ssdi8.dims(4, 4096, 80, 1), f16, "separate")
+    assert not use(ssdi8.dims(4, 4096, 80, 1), f32, "single")  # fp32 x: separate kernels
+    assert not use(ssdi8.dims(4, 4096, 80, 1), f16, "single", taps=("state_in_q",))
+    assert use(ssdi8.dims(4, 4096, 80, 1), f16, "single", taps=("cb_q",))   # ChunkBMM taps ok
+    assert not use(ssdi8.dims(4, 300, 80, 1), f16, "single")   # invalid sizes
+
+
+def test_scan_path_out_of_range(ssdi8):
+    L = ssdi8.lib()
+    d = ssdi8.dims(2, 512, 8, 2)
+    a = ssdi8.ScanArgs()
+    for f in ("x", "dt", "A", "Bq", "Cq", "B_scale", "C_scale", "xs_scale", "state_scale",
+              "cb_scale", "y", "workspace"):
+        setattr(a, f, A16)
+    a.x_dtype = a.y_dtype = ssdi8.F16
+    a.decay_shift, a.workspace_bytes = 7, 1 << 40
+    a.path = 3
+    assert L.ssdi8_ssd_chunk_scan(ctypes.byref(d), ctypes.byref(a), None) == ssdi8.ERR_ARG
