@@ -71,7 +71,7 @@ Fp16Plan plan_fp16(const ssdi8_dims* d) {
 struct CalibPlan {
   Fp16Plan f16;
   Plan i8;
-  size_t f16_base, i8_base, bq, cq, yfp, yq, dec64, amax, total;
+  size_t f16_base, i8_base, bq, cq, yfp, yq, dec64, amax, part, total;
 };
 
 // Calibration workspace: the FP16 layer's and the INT8 layer's workspaces, the quantized B and C,
@@ -93,6 +93,7 @@ CalibPlan plan_calib(const ssdi8_dims* d) {
   p.yq = off;       off = round_up(off + 4 * B * L * H * P, 256);
   p.dec64 = off;    off = round_up(off + 8 * B * H * nc, 256);
   p.amax = off;     off = round_up(off + 4 * (2 * H * P + G), 256);
+  p.part = off;     off = round_up(off + ssdi8::calib_corr_scratch_bytes((int)H), 256);
   p.total = off;
   return p;
 }
@@ -482,7 +483,8 @@ ssdi8_status ssdi8_calibrate(const ssdi8_dims* d, const ssdi8_calib_args* a, voi
     if (ls != SSDI8_OK) return ls;
   }
   if (e == hipSuccess)
-    e = ssdi8::launch_calib_corr(yfp, yq, a->corr, d->batch * d->seqlen, H, a->eta, st);
+    e = ssdi8::launch_calib_corr(yfp, yq, reinterpret_cast<double*>(ws + plan.part), a->corr,
+                                 d->batch * d->seqlen, H, a->eta, st);
   return e == hipSuccess ? SSDI8_OK : SSDI8_ERR_HIP;
 }
 

@@ -245,26 +245,38 @@ __global__ void calib_steps_kernel(const uint32_t* __restrict__ xs_amax,
   }
 }
 
-// ---- corr[h, p] = eta * mean over (b, l) of (y_fp - y_q); one workgroup per head, fp64 sums
-__global__ __launch_bounds__(256) void calib_corr_kernel(const float* __restrict__ y_fp,
-                                                         const float* __restrict__ y_q,
-                                                         float* __restrict__ corr, int64_t T,
-                                                         int H, float eta) {
+// ---- corr[h, p] = eta * mean over (b, l) of (y_fp - y_q), in fp64 and in a fixed order: stage 1
+//      sums token block nb of head h (blockIdx = (h, nb)) per channel, stage 2 adds the blocks
+constexpr int kCorrBlocks = 64;
+
+__global__ __launch_bounds__(256) void calib_corr_partial(const float* __restrict__ y_fp,
+                                                          const float* __restrict__ y_q,
+                                                          double* __restrict__ part, int64_t T,
+                                                          int H) {
   __shared__ double s_sum[4][kP];
-  const int t = threadIdx.x, p = t & 63, part = t >> 6;
-  const int h = blockIdx.x;
+  const int t = threadIdx.x, p = t & 63, q = t >> 6;
+  const int h = blockIdx.x, nb = blockIdx.y, nbs = gridDim.y;
+  const int64_t t0 = T * nb / nbs, t1 = T * (nb + 1) / nbs;
   const size_t HP = (size_t)H * kP;
   double sum = 0.0;
-  for (int64_t tok = part; tok < T; tok += 4) {
+  for (int64_t tok = t0 + q; tok < t1; tok += 4) {
     const size_t i = (size_t)tok * HP + (size_t)h * kP + p;
     sum += (double)y_fp[i] - (double)y_q[i];
   }
-  s_sum[part][p] = sum;
+  s_sum[q][p] = sum;
   __syncthreads();
-  if (t < kP) {
-    const double s = s_sum[0][t] + s_sum[1][t] + s_sum[2][t] + s_sum[3][t];
-    corr[h * kP + t] = (float)((double)eta * s / (double)T);
-  }
+  if (t < kP)
+    part[((size_t)h * nbs + nb) * kP + t] = s_sum[0][t] + s_sum[1][t] + s_sum[2][t] + s_sum[3][t];
+}
+
+__global__ void calib_corr_final(const double* __restrict__ part, float* __restrict__ corr,
+                                 int64_t T, int H, int nbs, float eta) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= H * kP) return;
+  const int h = i / kP, p = i - h * kP;
+  double s = 0.0;
+  for (int nb = 0; nb < nbs; ++nb) s += part[((size_t)h * nbs + nb) * kP + p];
+  corr[i] = (float)((double)eta * s / (double)T);
 }
 
 __global__ void zero_u32(uint32_t* p, int n) {
@@ -323,10 +335,15 @@ hipError_t launch_calib_steps(const uint32_t* xs_amax, const uint32_t* s_amax,
   return hipGetLastError();
 }
 
-hipError_t launch_calib_corr(const float* y_fp, const float* y_q, float* corr, int64_t T, int H,
-                             float eta, hipStream_t st) {
-  hipLaunchKernelGGL(calib_corr_kernel, dim3((unsigned)H), dim3(256), 0, st, y_fp, y_q, corr, T,
-                     H, eta);
+size_t calib_corr_scratch_bytes(int H) { return (size_t)H * kCorrBlocks * kP * sizeof(double); }
+
+hipError_t launch_calib_corr(const float* y_fp, const float* y_q, double* part, float* corr,
+                             int64_t T, int H, float eta, hipStream_t st) {
+  const int64_t nb = T / 256 < 1 ? 1 : (T / 256 > kCorrBlocks ? kCorrBlocks : T / 256);
+  hipLaunchKernelGGL(calib_corr_partial, dim3((unsigned)H, (unsigned)nb), dim3(256), 0, st, y_fp,
+                     y_q, part, T, H);
+  hipLaunchKernelGGL(calib_corr_final, dim3((unsigned)((H * kP + 255) / 256)), dim3(256), 0, st,
+                     part, corr, T, H, (int)nb, eta);
   return hipGetLastError();
 }
 

@@ -124,23 +124,26 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
   const int wv = __builtin_amdgcn_readfirstlane(t >> 6);   // wave-uniform, so block loops are scalar
   int b, c, h;
   if constexpr (kFused) {
-    // Work items in ticket order.  The sequences (b, h) are dealt to 8 classes (bh % 8); class x
-    // hands out its items chunk-major from its own counter sync[x], so the item a workgroup
-    // waits for (same sequence, previous chunk) holds an earlier ticket of the same counter and
-    // is running or done.  A workgroup draws from class blockIdx % 8 (with round-robin dispatch
-    // over the 8 XCDs, a sequence stays on one XCD) and, once that class is exhausted, from the
-    // next ones; the grid has as many workgroups as items, so every item is drawn.
+    // Work items in ticket order.  The sequences (b, h) are split into 8 classes of consecutive
+    // sequences; class x hands out its items chunk-major from its own counter sync[x], so the
+    // item a workgroup waits for (same sequence, previous chunk) holds an earlier ticket of the
+    // same counter and is running or done.  A workgroup draws from class blockIdx % 8 (with
+    // round-robin dispatch over the 8 XCDs, a class stays on one XCD, where the heads of one
+    // batch element share the chunk's B_q^T, C_q and CB_q in L2) and, once that class is
+    // exhausted, from the next ones; the grid has as many workgroups as items, so every item
+    // is drawn.
     if (t == 0) {
       const int nbh = fs.nbh;
+      const int q = nbh / kSyncClasses, r = nbh - q * kSyncClasses;
       int item = -1;
       for (int k = 0; k < kSyncClasses && item < 0; ++k) {
         const int x = (int)((blockIdx.x + k) & (kSyncClasses - 1));
-        const int chains = (nbh - x + kSyncClasses - 1) / kSyncClasses;
+        const int chains = q + (x < r ? 1 : 0);
         if (chains <= 0) continue;
         const int tk = atomicAdd(fs.sync + x, 1);
         if (tk < chains * nc) {
           const int cc = tk / chains;
-          item = cc * nbh + x + kSyncClasses * (tk - cc * chains);
+          item = cc * nbh + x * q + (x < r ? x : r) + (tk - cc * chains);
         }
       }
       sm.misc[0] = item;
@@ -309,7 +312,6 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
         }
         __builtin_amdgcn_s_sleep(2);
       }
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
       if (!ok) atomicAdd(fs.sync + kSyncClasses, 1);
     }
     __syncthreads();
@@ -324,8 +326,9 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
         const size_t rbase = (size_t)bh * kSlab + (size_t)prow * kN + 32 * (ntb + i) + 4 * hf;
         uint32_t cw[4];
         if (c > 0) {
-          const uint4 v = *reinterpret_cast<const uint4*>(slab + off);
-          cw[0] = v.x; cw[1] = v.y; cw[2] = v.z; cw[3] = v.w;
+          // sc1: read at the agent's coherence point (written there by the publisher)
+          const auto v = __builtin_amdgcn_raw_buffer_load_b128(buffer_rsrc(slab), (int)off, 0, 16);
+          cw[0] = v[0]; cw[1] = v[1]; cw[2] = v[2]; cw[3] = v[3];
         } else {
 #pragma unroll
           for (int g4 = 0; g4 < 4; ++g4)

@@ -120,7 +120,8 @@ hipError_t launch_calib_states(const LayerDims& d, const void* x, int x_dtype, c
 hipError_t launch_calib_steps(const uint32_t* xs_amax, const uint32_t* s_amax,
                               const uint32_t* cb_amax, float* aXs, float* aS, float* aCB, int H,
                               int G, int xs_per_head, hipStream_t st);
-hipError_t launch_calib_corr(const float* y_fp, const float* y_q, float* corr, int64_t T, int H,
-                             float eta, hipStream_t st);
+size_t calib_corr_scratch_bytes(int H);
+hipError_t launch_calib_corr(const float* y_fp, const float* y_q, double* part, float* corr,
+                             int64_t T, int H, float eta, hipStream_t st);
 
 }  // namespace ssdi8

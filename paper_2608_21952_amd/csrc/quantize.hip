@@ -73,6 +73,52 @@ __global__ __launch_bounds__(256) void quant_static_vec16(const T* __restrict__ 
   }
 }
 
+// fp16 source, m % 8 == 0: units of 8 consecutive elements (one 16-byte load, one 8-byte
+// store), lane-contiguous so that a wave's loads cover one contiguous 1 KB; kU units per thread
+// in flight.  32-bit indices (n < 2^31).
+template <int kU>
+__global__ __launch_bounds__(256) void quant_static_h8(const _Float16* __restrict__ src,
+                                                      int8_t* __restrict__ dst,
+                                                      const float* __restrict__ scale, int gran,
+                                                      uint32_t nunit, uint32_t k, uint32_t m) {
+  const uint32_t rowunits = m / 8;
+  const uint32_t u0 = blockIdx.x * (256u * kU) + threadIdx.x;
+  uint4 raw[kU];
+#pragma unroll
+  for (int u = 0; u < kU; ++u) {
+    const uint32_t unit = u0 + 256u * u;
+    if (unit < nunit) raw[u] = reinterpret_cast<const uint4*>(src)[unit];
+  }
+#pragma unroll
+  for (int u = 0; u < kU; ++u) {
+    const uint32_t unit = u0 + 256u * u;
+    if (unit >= nunit) break;
+    const uint32_t row = unit / rowunits;
+    const uint32_t w[4] = {raw[u].x, raw[u].y, raw[u].z, raw[u].w};
+    int q[8];
+    if (gran == 2) {
+      const uint32_t c0 = (row % k) * m + (unit - row * rowunits) * 8;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const float x = (float)__builtin_bit_cast(
+            _Float16, (uint16_t)((i & 1) ? (w[i >> 1] >> 16) : (w[i >> 1] & 0xffffu)));
+        q[i] = quant_i8(x, 1.0f / scale[c0 + i]);
+      }
+    } else {
+      const uint32_t gi = gran == 0 ? 0u : (gran == 1 ? row % k : row);
+      const float inv = 1.0f / scale[gi];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const float x = (float)__builtin_bit_cast(
+            _Float16, (uint16_t)((i & 1) ? (w[i >> 1] >> 16) : (w[i >> 1] & 0xffffu)));
+        q[i] = quant_i8(x, inv);
+      }
+    }
+    reinterpret_cast<uint2*>(dst)[unit] =
+        make_uint2(pack4_i8(q[0], q[1], q[2], q[3]), pack4_i8(q[4], q[5], q[6], q[7]));
+  }
+}
+
 template <typename T>
 __global__ __launch_bounds__(256) void quant_static_scalar(const T* __restrict__ src,
                                                            int8_t* __restrict__ dst,
@@ -171,7 +217,13 @@ hipError_t quantize_impl(const T* src, int64_t b, int64_t l, int64_t k, int64_t 
                        scale, ngran);
   }
   if (n == 0) return hipGetLastError();
-  if (m % 16 == 0) {
+  if (sizeof(T) == 2 && m % 8 == 0 && n < ((int64_t)1 << 31)) {
+    constexpr int kU = 4;
+    const int64_t nunit = n / 8;
+    hipLaunchKernelGGL(quant_static_h8<kU>, dim3((unsigned)((nunit + 256 * kU - 1) / (256 * kU))),
+                       dim3(256), 0, st, reinterpret_cast<const _Float16*>(src), dst, scale, gran,
+                       (uint32_t)nunit, (uint32_t)k, (uint32_t)m);
+  } else if (m % 16 == 0) {
     const int64_t nvec = n / 16;
     if (n < ((int64_t)1 << 31)) {
       hipLaunchKernelGGL((quant_static_vec16<T, uint32_t>), dim3((unsigned)grid_for(nvec)),
