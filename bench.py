@@ -127,10 +127,42 @@ def cpu_baseline(cfg, inp, sc, budget_s: float):
     whole = nb == cfg.batch and nh == cfg.nheads
     what = ("the whole workload" if whole else
             f"batch elements 0..{nb - 1} of {cfg.batch}, heads 0..{nh - 1} of {cfg.nheads}")
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
     return {"value": tokens / t, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "cpu_model": model,
             "sample": f"{what}, {cfg.seqlen} tokens each ({t:.1f} s; tokens/s counted as layer "
                       f"tokens = token-heads / {cfg.nheads})",
             "seconds": round(t, 2), "host_cpus": len(os.sched_getaffinity(0))}
+
+
+def measured_peaks(torch, ssdi8):
+    """On-box peaks: a 1 GiB device-to-device copy (bytes read + written per second) and the
+    MFMA probe loops (int8, fp16), best of a few runs."""
+    n = 1 << 30
+    src = torch.ones(n, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    best = 0.0
+    for _ in range(4):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        dst.copy_(src)
+        e1.record()
+        torch.cuda.synchronize()
+        best = max(best, 2 * n / (e0.elapsed_time(e1) * 1e-3) / 1e9)
+    del src, dst
+    return {"hbm_copy_GBps": round(best, 1),
+            "int8_mfma_TOPS": round(ssdi8.mfma_peak("int8") / 1e12, 1),
+            "fp16_mfma_TFLOPS": round(ssdi8.mfma_peak("fp16") / 1e12, 1),
+            "how": "1 GiB device copy (read + write bytes); 1024 workgroups x 4 waves x 4 "
+                   "independent MFMA chains on register operands (ssdi8_mfma_probe)"}
 
 
 def queue_ahead(torch, K):
@@ -351,6 +383,19 @@ def main():
     torch.cuda.synchronize()
     total_ms = t0.elapsed_time(t1)
     ms_step = total_ms / K
+    # the median over K more steps, each bracketed by its own events (an event between steps
+    # adds a little, so the mean above comes from the uninterrupted run)
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(K + 1)]
+    marks[0].record()
+    for k in range(K):
+        if graph is not None:
+            graph.replay()
+        else:
+            step()
+        marks[k + 1].record()
+    torch.cuda.synchronize()
+    per_step = sorted(marks[k].elapsed_time(marks[k + 1]) for k in range(K))
+    ms_median = per_step[K // 2] if K % 2 else 0.5 * (per_step[K // 2 - 1] + per_step[K // 2])
     if graph is not None:
         # per-kernel durations: K eager steps right after, with HIP events recorded on the
         # launch stream between the kernels (same kernels; an event record adds ~1-3 us)
@@ -401,7 +446,8 @@ def main():
     result = {
         "metric": "INT8 SSD chunk-scan tokens/s per layer",
         "value": value, "unit": "tokens/s", "n_gpus": 1, "steps": K, "warmup": W,
-        "ms_per_step": ms_step, "higher_is_better": True, "scaling": "weak",
+        "ms_per_step": ms_step, "ms_per_step_median": ms_median,
+        "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "int8+fp16", "data": "synthetic",
         "config": {"workload": cfg.name, "batch": cfg.batch, "seqlen": cfg.seqlen,
                    "nheads": cfg.nheads, "headdim": cfg.headdim, "dstate": cfg.dstate,
@@ -422,6 +468,52 @@ def main():
     result["fp16_baseline"] = f16
     result["decode"] = time_decode(torch, ssdi8, cfg, inp, sc, K, W)
     result["calibrate"] = time_calibrate(torch, ssdi8, cfg, x, dt, A, Bf, Cf, D, min(K, 5))
+    # cold: every step after a 512 MiB scratch write that evicts the 256 MB Infinity Cache
+    Kc = min(K, 20)
+    scratch = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    cold_ms, cold_dom = [], []
+    for k in range(Kc):
+        scratch.fill_(k & 0xff)
+        c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        c0.record()
+        if graph is not None:
+            graph.replay()
+        else:
+            step()
+        c1.record()
+        torch.cuda.synchronize()
+        cold_ms.append(c0.elapsed_time(c1))
+    ev2 = ssdi8.HipEvents(7 * Kc)
+    for k in range(Kc):
+        scratch.fill_(k & 0xff)
+        ev2.record(7 * k)
+        ssdi8.quantize_act(Bf, "group", aB, out=Bq)
+        ev2.record(7 * k + 1)
+        ssdi8.quantize_act(Cf, "group", aC, out=Cq)
+        ssdi8.ssd_chunk_scan(x, dt, A, Bq, Cq, aB, aC, aXs, aS, aCB, D=D, corr=corr,
+                             workspace=ws, y=y, final_state=True, path=args.path,
+                             stage_events=ev2.group(7 * k + 2))
+        torch.cuda.synchronize()
+        # the dominant kernel (ChunkScan, or the single pass) runs between events 3 and 4
+        cold_dom.append(ev2.elapsed_ms(7 * k + 5, 7 * k + 6))
+    ev2.close()
+    del scratch
+    cms = sorted(cold_ms)[Kc // 2]
+    cdom = sorted(cold_dom)[Kc // 2]
+    result["cold"] = {
+        "what": "median of %d steps, each after a 512 MiB scratch write (Infinity Cache evicted)"
+                % Kc,
+        "ms_per_step": round(cms, 4), "tokens_per_s": tokens / (cms * 1e-3),
+        "dominant_kernel_us": round(cdom * 1e3, 2),
+        "dominant_kernel_GBps": round(abytes[dom] / (cdom * 1e-3) / 1e9, 1),
+        "dominant_kernel_hbm_frac": round(abytes[dom] / (cdom * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+    peaks = measured_peaks(torch, ssdi8)
+    result["measured_peaks"] = peaks
+    result["roofline"]["frac_of_measured_copy"] = round(ach / peaks["hbm_copy_GBps"], 4)
+    for n, st in stages.items():
+        st["frac_of_measured_copy"] = round(st["GBps"] / peaks["hbm_copy_GBps"], 4)
+        if "int8_tops" in st:
+            st["int8_frac_of_measured"] = round(st["int8_tops"] / peaks["int8_mfma_TOPS"], 4)
     if args.copy_probe_mb > 0:
         n = args.copy_probe_mb << 20
         src = torch.ones(n, dtype=torch.uint8, device="cuda")
@@ -433,6 +525,7 @@ def main():
         print("[bench] timing the CPU oracle on a bounded sample ...", file=sys.stderr,
               flush=True)
         cb = cpu_baseline(cfg, inp, sc, args.cpu_budget_s)
+        cb["gpu_over_cpu"] = round(value / cb["value"], 1)
         result["cpu_baseline"] = cb
     print(json.dumps(result), flush=True)
 

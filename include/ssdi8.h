@@ -282,6 +282,19 @@ typedef struct {
 size_t ssdi8_calibrate_workspace_size(const ssdi8_dims* d);
 ssdi8_status ssdi8_calibrate(const ssdi8_dims* d, const ssdi8_calib_args* a, void* stream);
 
+/*
+ * ssdi8_mfma_probe — measurement helper: the on-box peak rate of the matrix cores, the
+ * denominator of a "fraction of measured MFMA peak" beside the datasheet one.  Launches `blocks`
+ * workgroups (1..65535) of 4 wavefronts; each wavefront runs 4 independent chains of `iters`
+ * MFMAs on register operands (int8 v_mfma_i32_32x32x32_i8 for SSDI8_PROBE_I8, fp16
+ * v_mfma_f32_32x32x16_f16 for SSDI8_PROBE_F16).  out: device, 256·blocks int32 (int8) or fp32
+ * values (written, meaningless).  *ops (host, may be NULL) receives the multiply-add count × 2 of
+ * the launch; time it with events on `stream`.
+ */
+typedef enum { SSDI8_PROBE_I8 = 0, SSDI8_PROBE_F16 = 1 } ssdi8_probe_kind;
+ssdi8_status ssdi8_mfma_probe(int kind, int64_t iters, int64_t blocks, void* out, int64_t* ops,
+                              void* stream);
+
 /* Static description of a status code. */
 const char* ssdi8_status_string(int status);
 

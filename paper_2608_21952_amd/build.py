@@ -23,7 +23,7 @@ LIB = os.path.join(PKG, "libssdi8.so")
 ARCH = "gfx950"
 SOURCES = ["api.hip", "quantize.hip", "chunk_bmm.hip", "chunk_state.hip", "state_pass.hip",
            "chunk_scan.hip", "decode.hip", "fp16_bmm.hip", "fp16_state.hip",
-           "fp16_scan.hip", "calibrate.hip"]
+           "fp16_scan.hip", "calibrate.hip", "probe.hip"]
 
 # -ffp-contract=off: no fused multiply-add where the arithmetic defines separate roundings.
 # -packed-fp32-ops off: never emit packed fp32 arithmetic.

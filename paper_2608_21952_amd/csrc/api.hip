@@ -488,6 +488,18 @@ ssdi8_status ssdi8_calibrate(const ssdi8_dims* d, const ssdi8_calib_args* a, voi
   return e == hipSuccess ? SSDI8_OK : SSDI8_ERR_HIP;
 }
 
+ssdi8_status ssdi8_mfma_probe(int kind, int64_t iters, int64_t blocks, void* out,
+                              int64_t* ops, void* stream) {
+  if (kind != SSDI8_PROBE_I8 && kind != SSDI8_PROBE_F16) return SSDI8_ERR_ARG;
+  if (iters < 1 || blocks < 1 || blocks > 65535 || iters > ((int64_t)1 << 40)) return SSDI8_ERR_ARG;
+  if (!out) return SSDI8_ERR_NULL;
+  if (((uintptr_t)out & 3u) != 0) return SSDI8_ERR_ALIGN;
+  if (ops) *ops = ssdi8::mfma_probe_ops(kind, iters, blocks);
+  if (ssdi8::launch_mfma_probe(kind, iters, blocks, out, (hipStream_t)stream) != hipSuccess)
+    return SSDI8_ERR_HIP;
+  return SSDI8_OK;
+}
+
 ssdi8_status ssdi8_decode_step(int64_t batch, int64_t nheads, int64_t headdim, int64_t ngroups,
                                int64_t dstate, const ssdi8_decode_args* a, void* stream) {
   if (batch < 0 || nheads < 1 || headdim < 1 || ngroups < 1 || dstate < 1) return SSDI8_ERR_SHAPE;

@@ -49,8 +49,10 @@ template <> struct Pair<float> {
   static __device__ __forceinline__ float hi(raw v) { return v.y; }
 };
 
+// fp16 x: at most 80 VGPRs, six workgroups per CU (a 130M-shaped layer's 1536 chunk items fit
+// in one round); the fp32-x form keeps four
 template <typename XT>
-__global__ __launch_bounds__(256) void chunk_state_kernel(
+__global__ __launch_bounds__(256, sizeof(XT) == 2 ? 6 : 4) void chunk_state_kernel(
     const XT* __restrict__ x, const float* __restrict__ dt, const float* __restrict__ A,
     const int8_t* __restrict__ bqT, const float* __restrict__ B_scale,
     const float* __restrict__ xs_scale, int xs_per_head, const float* __restrict__ state_scale,
@@ -104,18 +106,20 @@ __global__ __launch_bounds__(256) void chunk_state_kernel(
   // ---- X_scaled -> X_q, written transposed to LDS ([p][j], tokens contiguous)
   {
     const float inv0 = s_inv[p0], inv1 = s_inv[p0 + 1];
+    // quantized and packed 4 token rows at a time, so that the raw rows die as they are used
     uint32_t w0[8], w1[8];
-    int qa[32], qb[32];
-#pragma unroll
-    for (int r = 0; r < 32; ++r) {
-      const float lut = s_lut[jb * 32 + r];
-      qa[r] = quant_i8(lut * Pair<XT>::lo(xr[r]), inv0);
-      qb[r] = quant_i8(lut * Pair<XT>::hi(xr[r]), inv1);
-    }
 #pragma unroll
     for (int r4 = 0; r4 < 8; ++r4) {
-      w0[r4] = pack4_i8(qa[4 * r4], qa[4 * r4 + 1], qa[4 * r4 + 2], qa[4 * r4 + 3]);
-      w1[r4] = pack4_i8(qb[4 * r4], qb[4 * r4 + 1], qb[4 * r4 + 2], qb[4 * r4 + 3]);
+      int qa[4], qb[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int r = 4 * r4 + i;
+        const float lut = s_lut[jb * 32 + r];
+        qa[i] = quant_i8(lut * Pair<XT>::lo(xr[r]), inv0);
+        qb[i] = quant_i8(lut * Pair<XT>::hi(xr[r]), inv1);
+      }
+      w0[r4] = pack4_i8(qa[0], qa[1], qa[2], qa[3]);
+      w1[r4] = pack4_i8(qb[0], qb[1], qb[2], qb[3]);
     }
     int8_t* r0 = s_xq + p0 * kXS + jb * 32;
     int8_t* r1 = r0 + kXS;
@@ -128,7 +132,8 @@ __global__ __launch_bounds__(256) void chunk_state_kernel(
 #pragma unroll
       for (int r = 0; r < 32; ++r)
         *reinterpret_cast<uint16_t*>(tb + (size_t)r * HP) =
-            (uint16_t)((qa[r] & 0xff) | ((qb[r] & 0xff) << 8));
+            (uint16_t)(((w0[r >> 2] >> (8 * (r & 3))) & 0xffu) |
+                       (((w1[r >> 2] >> (8 * (r & 3))) & 0xffu) << 8));
     }
   }
   __syncthreads();
@@ -142,7 +147,7 @@ __global__ __launch_bounds__(256) void chunk_state_kernel(
     // B_q^T fragments of n-tiles ntb, ntb + 1: 1 KB per (n-tile, 32-token block), lane-major
     const int8_t* b0f = bq + (size_t)ntb * (kQ / 32) * 1024 + lane * 16;
     const int8_t* b1f = b0f + (size_t)(kQ / 32) * 1024;
-#pragma unroll
+#pragma unroll 4
     for (int ks = 0; ks < kQ / 32; ++ks) {
       const int kof = ks * 32 + 16 * (lane >> 5);
       const v4i a = *reinterpret_cast<const v4i*>(arow + kof);

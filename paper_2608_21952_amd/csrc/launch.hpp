@@ -124,4 +124,9 @@ size_t calib_corr_scratch_bytes(int H);
 hipError_t launch_calib_corr(const float* y_fp, const float* y_q, double* part, float* corr,
                              int64_t T, int H, float eta, hipStream_t st);
 
+// MFMA peak probe (int8 32x32x32 for dtype 0, fp16 32x32x16 otherwise): `blocks` workgroups of
+// 4 waves, each running 4 independent chains of `iters` MFMAs; one value per thread to `out`.
+int64_t mfma_probe_ops(int dtype, int64_t iters, int64_t blocks);
+hipError_t launch_mfma_probe(int dtype, int64_t iters, int64_t blocks, void* out, hipStream_t st);
+
 }  // namespace ssdi8

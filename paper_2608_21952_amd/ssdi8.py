@@ -118,6 +118,9 @@ def lib() -> ctypes.CDLL:
     L.ssdi8_calibrate_workspace_size.restype = ctypes.c_size_t
     L.ssdi8_calibrate.argtypes = [ctypes.POINTER(Dims), ctypes.POINTER(CalibArgs), _P]
     L.ssdi8_calibrate.restype = _I
+    L.ssdi8_mfma_probe.argtypes = [_I, ctypes.c_int64, ctypes.c_int64, _P,
+                                   ctypes.POINTER(ctypes.c_int64), _P]
+    L.ssdi8_mfma_probe.restype = _I
     L.ssdi8_status_string.argtypes = [_I]
     L.ssdi8_status_string.restype = ctypes.c_char_p
     L.ssdi8_version.argtypes = []
@@ -383,6 +386,24 @@ def uses_single_pass(d: Dims, x_dtype: torch.dtype, path: str = "auto", taps=())
     for name in taps:
         setattr(a, name, 16)      # a non-NULL tap pointer (only its presence matters here)
     return bool(lib().ssdi8_uses_single_pass(ctypes.byref(d), ctypes.byref(a)))
+
+
+def mfma_peak(kind: str = "int8", iters: int = 20000, blocks: int = 1024, reps: int = 3) -> float:
+    """Measured MFMA rate of this GPU (ops/s; ssdi8_mfma_probe), best of `reps` launches."""
+    out = torch.empty(blocks * 256, dtype=torch.int32 if kind == "int8" else torch.float32,
+                      device="cuda")
+    ops = ctypes.c_int64()
+    k = 0 if kind == "int8" else 1
+    best = 0.0
+    for _ in range(reps + 1):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        st = lib().ssdi8_mfma_probe(k, iters, blocks, _ptr(out), ctypes.byref(ops), _stream(None))
+        e1.record()
+        _check(st, "ssdi8_mfma_probe")
+        torch.cuda.synchronize()
+        best = max(best, ops.value / (e0.elapsed_time(e1) * 1e-3))
+    return best
 
 
 def fp16_workspace_size(d: Dims) -> int:

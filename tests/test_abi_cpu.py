@@ -359,3 +359,14 @@ def test_scan_path_out_of_range(ssdi8):
     a.decay_shift, a.workspace_bytes = 7, 1 << 40
     a.path = 3
     assert L.ssdi8_ssd_chunk_scan(ctypes.byref(d), ctypes.byref(a), None) == ssdi8.ERR_ARG
+
+
+def test_mfma_probe_argument_errors(ssdi8):
+    L = ssdi8.lib()
+    ops = ctypes.c_int64()
+    assert L.ssdi8_mfma_probe(2, 10, 4, A16, ctypes.byref(ops), None) == ssdi8.ERR_ARG
+    assert L.ssdi8_mfma_probe(0, 0, 4, A16, ctypes.byref(ops), None) == ssdi8.ERR_ARG
+    assert L.ssdi8_mfma_probe(0, 10, 0, A16, ctypes.byref(ops), None) == ssdi8.ERR_ARG
+    assert L.ssdi8_mfma_probe(0, 10, 70000, A16, ctypes.byref(ops), None) == ssdi8.ERR_ARG
+    assert L.ssdi8_mfma_probe(0, 10, 4, None, ctypes.byref(ops), None) == ssdi8.ERR_NULL
+    assert L.ssdi8_mfma_probe(1, 10, 4, A16 + 2, ctypes.byref(ops), None) == ssdi8.ERR_ALIGN

@@ -322,3 +322,17 @@ def test_graph_replay_matches_eager(torch, ssdi8):
         assert np.array_equal(y.cpu().numpy(), eager["y"]), f"replay {rep}: y differs"
         assert np.array_equal(out["state_in_q"].cpu().numpy(), eager["state_in_q"]), rep
         assert np.array_equal(out["final_state_q"].cpu().numpy(), eager["final_state_q"]), rep
+
+
+def test_mfma_probe_counts_and_runs(torch, ssdi8):
+    """The measurement helper: its op count is the launch's (workgroups x 4 waves x 4 chains x
+    iterations x 2 M N K) and it runs to completion for both kinds."""
+    import ctypes
+    for kind, mnk in ((0, 32 * 32 * 32), (1, 32 * 32 * 16)):
+        out = torch.zeros(8 * 256, dtype=torch.int32 if kind == 0 else torch.float32,
+                          device="cuda")
+        ops = ctypes.c_int64()
+        st = ssdi8.lib().ssdi8_mfma_probe(kind, 100, 8, out.data_ptr(), ctypes.byref(ops), None)
+        torch.cuda.synchronize()
+        assert st == 0 and ops.value == 8 * 4 * 4 * 100 * 2 * mnk
+    assert ssdi8.mfma_peak("int8", iters=200, blocks=256, reps=1) > 0
