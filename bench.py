@@ -2,8 +2,9 @@
 """Throughput of the SSDi8 INT8 SSD chunk scan (one SSD layer) on one MI355X.
 
 A step is one whole layer on one batch of synthetic Mamba-2-shaped input already resident in
-HBM: quantize B and C per group (ssdi8_quantize_act x 2) and ssdi8_ssd_chunk_scan (ChunkBMM,
-ChunkCumsum + ChunkState, StatePassing, ChunkScan 1+2 with the D skip and the correction).
+HBM: ssdi8_ssd_chunk_scan on the unquantized B and C (ChunkBMM quantizes them per group with the
+static steps, then ChunkCumsum + ChunkState, StatePassing, ChunkScan 1+2 with the D skip and the
+correction; --separate-quant times ssdi8_quantize_act x 2 + the scan on B_q, C_q instead).
 Scales are static (calibrated offline by the CPU oracle; stored in tests/golden/calib).
 
 Prints ONE JSON line: tokens/s per layer, ms/step, the roofline of the dominant kernel measured
@@ -29,8 +30,9 @@ SINGLE = ("chunk_bmm", "single_pass")
 SOURCE = {"single_pass": "chunk_scan"}      # kernel -> source file of its HIP code
 
 
-def algorithmic_bytes(cfg):
-    """Minimum HBM bytes each kernel must move for its inputs and outputs (per launch)."""
+def algorithmic_bytes(cfg, quant_in_bmm=False):
+    """Minimum HBM bytes each kernel must move for its inputs and outputs (per launch); with
+    quant_in_bmm ChunkBMM reads the unquantized B and C."""
     B, L, H, P, G, N, Q = (cfg.batch, cfg.seqlen, cfg.nheads, cfg.headdim, cfg.ngroups,
                            cfg.dstate, cfg.chunk)
     T, c = B * L, L // Q
@@ -40,7 +42,7 @@ def algorithmic_bytes(cfg):
     return {
         "quantize_B": T * G * N * (sx + 1),
         "quantize_C": T * G * N * (sx + 1),
-        "chunk_bmm": 2 * T * G * N + cb_causal,
+        "chunk_bmm": 2 * T * G * N * (sx if quant_in_bmm else 1) + cb_causal,
         "chunk_state": T * H * P * sx + T * H * 4 + T * G * N + states + B * H * c * 2,
         "state_pass": 2 * states + B * H * c * 2 + B * H * P * N * 5,
         "chunk_scan": 2 * T * H * P * sx + T * H * 4 + T * G * N + states + cb_causal,
@@ -304,6 +306,9 @@ def main():
     ap.add_argument("--path", choices=("auto", "separate", "single"), default="auto",
                     help="separate ChunkState / StatePassing / ChunkScan kernels, the single "
                          "pass, or the library's automatic choice")
+    ap.add_argument("--separate-quant", action="store_true",
+                    help="quantize B and C with ssdi8_quantize_act before the chunk scan (three "
+                         "calls) instead of handing them to ChunkBMM unquantized")
     ap.add_argument("--copy-probe-mb", type=int, default=0,
                     help="after the timed region, run one plain device-to-device copy of this "
                          "many MiB (a known-size reference for HBM byte counters)")
@@ -343,16 +348,28 @@ def main():
     K, W = args.steps, args.warmup
     ev = ssdi8.HipEvents(7 * max(K, 1))
 
-    def step(k=None):
-        if k is not None:
-            ev.record(7 * k)
-        ssdi8.quantize_act(Bf, "group", aB, out=Bq)
-        if k is not None:
-            ev.record(7 * k + 1)
-        ssdi8.quantize_act(Cf, "group", aC, out=Cq)
-        ssdi8.ssd_chunk_scan(x, dt, A, Bq, Cq, aB, aC, aXs, aS, aCB, D=D, corr=corr,
-                             workspace=ws, y=y, final_state=True, path=args.path,
-                             stage_events=None if k is None else ev.group(7 * k + 2))
+    def step(k=None, events=None):
+        events = ev if events is None else events
+        if args.separate_quant:
+            # ssdi8_quantize_act for B and C, then the chunk scan on B_q, C_q
+            if k is not None:
+                events.record(7 * k)
+            ssdi8.quantize_act(Bf, "group", aB, out=Bq)
+            if k is not None:
+                events.record(7 * k + 1)
+            ssdi8.quantize_act(Cf, "group", aC, out=Cq)
+            ssdi8.ssd_chunk_scan(x, dt, A, Bq, Cq, aB, aC, aXs, aS, aCB, D=D, corr=corr,
+                                 workspace=ws, y=y, final_state=True, path=args.path,
+                                 stage_events=None if k is None else events.group(7 * k + 2))
+        else:
+            # B and C handed over unquantized: ChunkBMM quantizes them with the static steps
+            if k is not None:
+                events.record(7 * k)
+                events.record(7 * k + 1)
+            ssdi8.ssd_chunk_scan(x, dt, A, None, None, aB, aC, aXs, aS, aCB, D=D, corr=corr,
+                                 workspace=ws, y=y, final_state=True, path=args.path,
+                                 B=Bf, C=Cf,
+                                 stage_events=None if k is None else events.group(7 * k + 2))
 
     for _ in range(W):
         step()
@@ -407,12 +424,13 @@ def main():
     single = ssdi8.uses_single_pass(ssdi8.dims(cfg.batch, cfg.seqlen, cfg.nheads, cfg.ngroups),
                                     x.dtype, args.path)
     mods = SINGLE if single else MODULES
-    names = ("quantize_B", "quantize_C") + mods
+    names = (("quantize_B", "quantize_C") if args.separate_quant else ()) + mods
     per = {n: 0.0 for n in names}
     for k in range(K):
         base = 7 * k
-        per["quantize_B"] += ev.elapsed_ms(base, base + 1)
-        per["quantize_C"] += ev.elapsed_ms(base + 1, base + 2)
+        if args.separate_quant:
+            per["quantize_B"] += ev.elapsed_ms(base, base + 1)
+            per["quantize_C"] += ev.elapsed_ms(base + 1, base + 2)
         if single:
             # events 1-3 are recorded back to back before the single pass
             per["chunk_bmm"] += ev.elapsed_ms(base + 2, base + 3)
@@ -422,7 +440,7 @@ def main():
                 per[n] += ev.elapsed_ms(base + 2 + i, base + 3 + i)
     per = {n: v / K for n, v in per.items()}
     ev.close()
-    abytes = algorithmic_bytes(cfg)
+    abytes = algorithmic_bytes(cfg, quant_in_bmm=not args.separate_quant)
     stages = {n: {"us": round(per[n] * 1e3, 2),
                   "GBps": round(abytes[n] / (per[n] * 1e-3) / 1e9, 1),
                   "hbm_frac": round(abytes[n] / (per[n] * 1e-3) / 1e9 / HBM_PEAK_GBS, 3)}
@@ -460,7 +478,9 @@ def main():
                    "bracketed by HIP events" if graph is not None else "eager launches"),
         "layer_hbm_frac": round(layer_min_bytes(cfg) / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "path": ("single pass: ChunkBMM, then ChunkState + StatePassing + ChunkScan in one kernel"
-                 if single else "separate ChunkBMM, ChunkState, StatePassing, ChunkScan kernels"),
+                 if single else "separate ChunkBMM, ChunkState, StatePassing, ChunkScan kernels")
+                + ("; B, C quantized by ssdi8_quantize_act first" if args.separate_quant
+                   else "; B, C quantized inside ChunkBMM"),
         "stages": stages,
     }
     f16 = time_fp16(torch, ssdi8, cfg, x, dt, A, Bf, Cf, D, K, W)
@@ -486,13 +506,7 @@ def main():
     ev2 = ssdi8.HipEvents(7 * Kc)
     for k in range(Kc):
         scratch.fill_(k & 0xff)
-        ev2.record(7 * k)
-        ssdi8.quantize_act(Bf, "group", aB, out=Bq)
-        ev2.record(7 * k + 1)
-        ssdi8.quantize_act(Cf, "group", aC, out=Cq)
-        ssdi8.ssd_chunk_scan(x, dt, A, Bq, Cq, aB, aC, aXs, aS, aCB, D=D, corr=corr,
-                             workspace=ws, y=y, final_state=True, path=args.path,
-                             stage_events=ev2.group(7 * k + 2))
+        step(k, events=ev2)
         torch.cuda.synchronize()
         # the dominant kernel (ChunkScan, or the single pass) runs between events 3 and 4
         cold_dom.append(ev2.elapsed_ms(7 * k + 5, 7 * k + 6))

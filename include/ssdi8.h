@@ -124,7 +124,8 @@ typedef struct {
                                       /*   (fp64, threshold 20, rounded once to fp32)            */
   const float* A;                     /* [H] decay parameter (<= 0)                              */
   const int8_t* Bq;                   /* [B,L,G,N] from ssdi8_quantize_act, per-group steps      */
-  const int8_t* Cq;                   /* [B,L,G,N] per-group steps, or per-token steps           */
+  const int8_t* Cq;                   /* [B,L,G,N] per-group steps, or per-token steps; or both  */
+                                      /*   NULL with B, C given unquantized (fields at the end)  */
   const float* B_scale;               /* [G]                                                     */
   const float* C_scale;               /* [G], or [B,L,G] when c_per_token != 0                   */
   int c_per_token;
@@ -165,6 +166,12 @@ typedef struct {
      chains bound it); 1: always the separate kernels; 2: the single pass whenever eligible.
      With the single pass, events 1-3 of stage_events are recorded back to back before it. */
   int path;
+  /* Alternative to Bq / Cq (both NULL then): the unquantized B, C [B,L,G,N] of bc_dtype
+     (SSDI8_F16 or SSDI8_F32), quantized inside ChunkBMM with the static steps B_scale, C_scale
+     (per group, or C per token with c_per_token) exactly as ssdi8_quantize_act does, so the
+     results are identical to quantizing first and passing Bq / Cq; the row-major int8 B, C
+     are then never written. */
+  const void* B; const void* C; int bc_dtype;
 } ssdi8_scan_args;
 
 /* Workspace bytes needed by ssdi8_ssd_chunk_scan for these sizes (0 on invalid sizes). */

@@ -215,11 +215,18 @@ ssdi8_status ssdi8_ssd_chunk_scan(const ssdi8_dims* d, const ssdi8_scan_args* a,
   if (a->decay_shift < 1 || a->decay_shift > 14) return SSDI8_ERR_ARG;
   if (a->path < 0 || a->path > 2) return SSDI8_ERR_ARG;
   const bool work = d->batch > 0 && d->seqlen > 0;
-  if (work && (!a->x || !a->dt || !a->A || !a->Bq || !a->Cq || !a->B_scale || !a->C_scale ||
+  // B, C: quantized (Bq, Cq) or unquantized (B, C with bc_dtype), not both, not a mix
+  const bool quantized = a->Bq || a->Cq;
+  if (quantized && (a->B || a->C)) return SSDI8_ERR_ARG;
+  if (!quantized && (a->B || a->C) && a->bc_dtype != SSDI8_F32 && a->bc_dtype != SSDI8_F16)
+    return SSDI8_ERR_ARG;
+  const void* Bsrc = quantized ? (const void*)a->Bq : a->B;
+  const void* Csrc = quantized ? (const void*)a->Cq : a->C;
+  if (work && (!a->x || !a->dt || !a->A || !Bsrc || !Csrc || !a->B_scale || !a->C_scale ||
                !a->xs_scale || !a->state_scale || !a->cb_scale || !a->y))
     return SSDI8_ERR_NULL;
   if (a->final_state && !a->state_scale) return SSDI8_ERR_NULL;
-  const void* al[] = {a->x, a->y, a->Bq, a->Cq, a->init_state_q, a->final_state_q,
+  const void* al[] = {a->x, a->y, a->Bq, a->Cq, a->B, a->C, a->init_state_q, a->final_state_q,
                       a->final_state, a->xs_q, a->state_i32, a->state_q, a->decay_q,
                       a->state_in_q, a->cb_i32, a->cb_q, a->scan1_i32, a->workspace};
   for (const void* p : al)
@@ -267,7 +274,8 @@ ssdi8_status ssdi8_ssd_chunk_scan(const ssdi8_dims* d, const ssdi8_scan_args* a,
   const bool fused = single_pass(d, a);
   int* sync = reinterpret_cast<int*>(ws + plan.sync);
   if (!mark(0)) return SSDI8_ERR_HIP;
-  hipError_t e = ssdi8::launch_chunk_bmm(ld, a->Cq, a->Bq, a->C_scale, a->c_per_token,
+  hipError_t e = ssdi8::launch_chunk_bmm(ld, Csrc, Bsrc, quantized ? -1 : a->bc_dtype,
+                                         a->C_scale, a->c_per_token,
                                          a->B_scale, a->cb_scale, cbq, a->cb_q, a->cb_i32, bqT,
                                          cq, fused ? 1 : 0, sync, fused ? (int)plan.nsync : 0,
                                          st);

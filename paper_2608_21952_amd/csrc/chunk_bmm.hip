@@ -12,6 +12,9 @@
 //          waves of the i = 0 blocks, which hold exactly those fragments in registers
 //   B_q^T  written by a tenth workgroup per chunk: ChunkState contracts over tokens and needs B
 //          with the token axis as the K-slice; every head of the group reuses it.
+// B and C may also arrive unquantized (fp16 / fp32) with static steps: each row is then quantized
+// as it is loaded (the B/C quantization of Eq. 1 fused into this kernel, which is the only reader
+// of the row-major B_q, C_q), with the arithmetic of ssdi8_quantize_act.
 #include "common.hpp"
 #include "frag.hpp"
 #include "launch.hpp"
@@ -24,11 +27,54 @@ constexpr int kBS = kN + 16;  // LDS row stride (bytes) of the staged B_q chunk
 constexpr int kTileWGs = 9;   // 36 causal 32x32 tiles = 9 workgroups x 4 waves
 constexpr int kRoles = kTileWGs + 1;
 
+// 16 consecutive K values of a B or C row as int8: already quantized (int8_t), or quantized here
+// from fp16 / fp32 with the static step exactly as ssdi8_quantize_act does (Eq. 1:
+// clamp(rne(fl32(v * fl32(1 / step))))).
+template <typename T> struct Row16;
+template <> struct Row16<int8_t> {
+  static __device__ __forceinline__ uint4 load(const int8_t* p, float) {
+    return *reinterpret_cast<const uint4*>(p);
+  }
+};
+template <> struct Row16<_Float16> {
+  static __device__ __forceinline__ uint4 load(const _Float16* p, float inv) {
+    const uint4 a = reinterpret_cast<const uint4*>(p)[0], b = reinterpret_cast<const uint4*>(p)[1];
+    const uint32_t w[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+    uint32_t o[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      int q[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const uint32_t wd = w[2 * i + (e >> 1)];
+        q[e] = quant_i8((float)__builtin_bit_cast(_Float16, (uint16_t)((e & 1) ? (wd >> 16)
+                                                                                : (wd & 0xffffu))),
+                        inv);
+      }
+      o[i] = pack4_i8(q[0], q[1], q[2], q[3]);
+    }
+    return make_uint4(o[0], o[1], o[2], o[3]);
+  }
+};
+template <> struct Row16<float> {
+  static __device__ __forceinline__ uint4 load(const float* p, float inv) {
+    uint32_t o[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float4 f = reinterpret_cast<const float4*>(p)[i];
+      o[i] = pack4_i8(quant_i8(f.x, inv), quant_i8(f.y, inv), quant_i8(f.z, inv),
+                      quant_i8(f.w, inv));
+    }
+    return make_uint4(o[0], o[1], o[2], o[3]);
+  }
+};
+
 // Work item w -> (b, c, g, role).  Roles 0..8 compute 4 causal tiles each (one per wave); role 9
 // writes B_q^T of the chunk.  The 10 workgroups of one chunk are consecutive work items, so the
 // XCD-aware mapping keeps them on one XCD where the 64 KB of B_q / C_q rows stay in L2.
+template <typename T>
 __global__ __launch_bounds__(256) void chunk_bmm_kernel(
-    const int8_t* __restrict__ Cq, const int8_t* __restrict__ Bq,
+    const T* __restrict__ Cq, const T* __restrict__ Bq,
     const float* __restrict__ C_scale, int c_per_token, const float* __restrict__ B_scale,
     const float* __restrict__ cb_scale, int8_t* __restrict__ cbq_frag,
     int8_t* __restrict__ cbq_tap, int32_t* __restrict__ cb32_tap, int8_t* __restrict__ bqT_frag,
@@ -48,8 +94,10 @@ __global__ __launch_bounds__(256) void chunk_bmm_kernel(
   const int b = bc / nc;
   const size_t tok0 = (size_t)b * L + (size_t)c * kQ;
   const size_t rs = (size_t)G * kN;  // token stride of B_q / C_q rows
-  const int8_t* cbase = Cq + tok0 * rs + (size_t)g * kN;
-  const int8_t* bbase = Bq + tok0 * rs + (size_t)g * kN;
+  const T* cbase = Cq + tok0 * rs + (size_t)g * kN;
+  const T* bbase = Bq + tok0 * rs + (size_t)g * kN;
+  // inverse steps for B, C given unquantized (per group; C per token with c_per_token)
+  const float inv_b = sizeof(T) == 1 ? 1.0f : 1.0f / B_scale[g];
   const size_t cg = ((size_t)b * nc + c) * G + g;   // chunk-group index
 
   if (role == kTileWGs) {
@@ -59,7 +107,7 @@ __global__ __launch_bounds__(256) void chunk_bmm_kernel(
       const int idx = it * 256 + t;
       const int j = idx >> 3, col = (idx & 7) * 16;
       *reinterpret_cast<uint4*>(s_b + j * kBS + col) =
-          *reinterpret_cast<const uint4*>(bbase + (size_t)j * rs + col);
+          Row16<T>::load(bbase + (size_t)j * rs + col, inv_b);
     }
     __syncthreads();
     // two units of 4 channels n x 16 tokens j per thread: 16 dword reads (4 bytes of n per
@@ -104,13 +152,16 @@ __global__ __launch_bounds__(256) void chunk_bmm_kernel(
   // ---- one causal 32x32 tile per wave
   int jt = 0, it = role * 4 + wv;
   while (it > jt) { it -= jt + 1; ++jt; }
-  const int8_t* arow = cbase + (size_t)(jt * 32 + (lane & 31)) * rs + 16 * (lane >> 5);
-  const int8_t* brow = bbase + (size_t)(it * 32 + (lane & 31)) * rs + 16 * (lane >> 5);
+  const T* arow = cbase + (size_t)(jt * 32 + (lane & 31)) * rs + 16 * (lane >> 5);
+  const T* brow = bbase + (size_t)(it * 32 + (lane & 31)) * rs + 16 * (lane >> 5);
+  float inv_c = 1.0f;
+  if constexpr (sizeof(T) != 1)
+    inv_c = 1.0f / (c_per_token ? C_scale[(tok0 + jt * 32 + (lane & 31)) * G + g] : C_scale[g]);
   v4i a[4], bb[4];
 #pragma unroll
   for (int ks = 0; ks < kN / 32; ++ks) {
-    a[ks] = *reinterpret_cast<const v4i*>(arow + 32 * ks);
-    bb[ks] = *reinterpret_cast<const v4i*>(brow + 32 * ks);
+    a[ks] = __builtin_bit_cast(v4i, Row16<T>::load(arow + 32 * ks, inv_c));
+    bb[ks] = __builtin_bit_cast(v4i, Row16<T>::load(brow + 32 * ks, inv_b));
   }
   if (it == 0) {
     // the C_q rows of block jt, in ChunkScan1 fragment order (before the MFMA chain, so that no
@@ -168,16 +219,22 @@ __global__ __launch_bounds__(256) void chunk_bmm_kernel(
 
 }  // namespace
 
-hipError_t launch_chunk_bmm(const LayerDims& d, const int8_t* Cq, const int8_t* Bq,
+hipError_t launch_chunk_bmm(const LayerDims& d, const void* C, const void* B, int src_dtype,
                             const float* C_scale, int c_per_token, const float* B_scale,
                             const float* cb_scale, int8_t* cbq_frag, int8_t* cbq_tap,
                             int32_t* cb32_tap, int8_t* bqT_frag, int8_t* cq_frag, int cq_perm,
                             int* sync, int nsync, hipStream_t st) {
   const int64_t nwork = (int64_t)d.batch * d.nchunks * d.ngroups * kRoles;
   if (nwork == 0) return hipSuccess;
-  hipLaunchKernelGGL(chunk_bmm_kernel, dim3((unsigned)nwork), dim3(256), 0, st, Cq, Bq, C_scale,
-                     c_per_token, B_scale, cb_scale, cbq_frag, cbq_tap, cb32_tap, bqT_frag,
-                     cq_frag, cq_perm, sync, nsync, d.seqlen, d.ngroups, d.nchunks);
+#define SSDI8_BMM_LAUNCH(T)                                                                     \
+  hipLaunchKernelGGL(chunk_bmm_kernel<T>, dim3((unsigned)nwork), dim3(256), 0, st,              \
+                     static_cast<const T*>(C), static_cast<const T*>(B), C_scale, c_per_token,  \
+                     B_scale, cb_scale, cbq_frag, cbq_tap, cb32_tap, bqT_frag, cq_frag,         \
+                     cq_perm, sync, nsync, d.seqlen, d.ngroups, d.nchunks)
+  if (src_dtype < 0) SSDI8_BMM_LAUNCH(int8_t);
+  else if (src_dtype == 1) SSDI8_BMM_LAUNCH(_Float16);
+  else SSDI8_BMM_LAUNCH(float);
+#undef SSDI8_BMM_LAUNCH
   return hipGetLastError();
 }
 

@@ -24,7 +24,9 @@ hipError_t launch_quantize(const void* src, int src_dtype, int64_t b, int64_t l,
 // kslice order, ChunkScan1; permuted kslice order with cq_perm, for the single pass).  The taps
 // are row-major [j][i].  sync[0, nsync) is cleared (the ticket and flags of
 // launch_chunk_scan_fused; nsync = 0 when that kernel does not follow).
-hipError_t launch_chunk_bmm(const LayerDims& d, const int8_t* Cq, const int8_t* Bq,
+// src_dtype < 0: C, B are the quantized int8 tensors; 1 / 0: unquantized fp16 / fp32, quantized
+// here with the static steps C_scale, B_scale exactly as launch_quantize does.
+hipError_t launch_chunk_bmm(const LayerDims& d, const void* C, const void* B, int src_dtype,
                             const float* C_scale, int c_per_token, const float* B_scale,
                             const float* cb_scale, int8_t* cbq_frag, int8_t* cbq_tap,
                             int32_t* cb32_tap, int8_t* bqT_frag, int8_t* cq_frag, int cq_perm,

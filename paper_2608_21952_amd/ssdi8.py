@@ -48,6 +48,7 @@ class ScanArgs(ctypes.Structure):
         ("cb_i32", _P), ("cb_q", _P), ("scan1_i32", _P),
         ("workspace", _P), ("workspace_bytes", ctypes.c_size_t),
         ("stage_events", _P), ("path", _I),
+        ("B", _P), ("C", _P), ("bc_dtype", _I),
     ]
 
 
@@ -248,8 +249,9 @@ TAPS = {  # name -> (dtype, shape builder(B, L, H, P, G, N, Q, c))
 }
 
 
-def ssd_chunk_scan(x: torch.Tensor, dt: torch.Tensor, A: torch.Tensor, Bq: torch.Tensor,
-                   Cq: torch.Tensor, B_scale: torch.Tensor, C_scale: torch.Tensor,
+def ssd_chunk_scan(x: torch.Tensor, dt: torch.Tensor, A: torch.Tensor,
+                   Bq: Optional[torch.Tensor], Cq: Optional[torch.Tensor],
+                   B_scale: torch.Tensor, C_scale: torch.Tensor,
                    xs_scale: torch.Tensor, state_scale: torch.Tensor, cb_scale: torch.Tensor, *,
                    D: Optional[torch.Tensor] = None, corr: Optional[torch.Tensor] = None,
                    dt_softplus: bool = True, chunk: int = CHUNK, decay_shift: int = 7,
@@ -257,20 +259,29 @@ def ssd_chunk_scan(x: torch.Tensor, dt: torch.Tensor, A: torch.Tensor, Bq: torch
                    y_dtype: Optional[torch.dtype] = None, final_state: bool = True,
                    taps: Iterable[str] = (), workspace: Optional[torch.Tensor] = None,
                    y: Optional[torch.Tensor] = None, stage_events=None,
-                   path: str = "auto", stream=None) -> Dict[str, torch.Tensor]:
+                   path: str = "auto", B: Optional[torch.Tensor] = None,
+                   C: Optional[torch.Tensor] = None, stream=None) -> Dict[str, torch.Tensor]:
     """One SSDi8 SSD layer (ssdi8_ssd_chunk_scan).  Shapes: x (B,L,H,P), dt (B,L,H), A (H),
-    Bq/Cq (B,L,G,N) int8, B_scale (G), C_scale (G) or (B,L,G) for per-token C steps,
+    Bq/Cq (B,L,G,N) int8 -- or Bq = Cq = None and B, C (B,L,G,N) fp16/fp32 unquantized, then
+    quantized with the static B_scale, C_scale inside ChunkBMM --, B_scale (G), C_scale (G) or
+    (B,L,G) for per-token C steps,
     xs_scale (H,P) or (H), state_scale (H,P), cb_scale (G), D (H), corr (H,P).
     Returns y, final_state_q, final_state and the requested taps (zero-initialised tensors,
     so entries a stage does not write, such as C.B^T above the diagonal, read as 0).
     path: "auto", "separate" (ChunkState, StatePassing, ChunkScan kernels) or "single" (the
     single-pass kernel whenever x is fp16 and no stage tap is requested)."""
     _need(x, "x")
+    Bsrc, Csrc = (Bq, Cq) if Bq is not None else (B, C)
     B, L, H, P = x.shape
-    _need(Bq, "Bq", torch.int8)
-    G, N = Bq.shape[2], Bq.shape[3]
-    _need(Bq, "Bq", torch.int8, (B, L, G, N))
-    _need(Cq, "Cq", torch.int8, (B, L, G, N))
+    if Bq is not None:
+        _need(Bq, "Bq", torch.int8)
+        if C is not None:
+            raise ValueError("pass either Bq, Cq or B, C")
+    elif Bsrc is None or Csrc is None:
+        raise ValueError("Bq, Cq or B, C are required")
+    G, N = Bsrc.shape[2], Bsrc.shape[3]
+    _need(Bsrc, "B", Bsrc.dtype, (B, L, G, N))
+    _need(Csrc, "C", Bsrc.dtype, (B, L, G, N))
     _need(dt, "dt", torch.float32, (B, L, H))
     _need(A, "A", torch.float32, (H,))
     _need(B_scale, "B_scale", torch.float32, (G,))
@@ -299,7 +310,11 @@ def ssd_chunk_scan(x: torch.Tensor, dt: torch.Tensor, A: torch.Tensor, Bq: torch
     a = ScanArgs()
     a.x, a.x_dtype = _ptr(x), _fdt(x)
     a.dt, a.dt_softplus, a.A = _ptr(dt), int(dt_softplus), _ptr(A)
-    a.Bq, a.Cq, a.B_scale, a.C_scale = _ptr(Bq), _ptr(Cq), _ptr(B_scale), _ptr(C_scale)
+    if Bq is not None:
+        a.Bq, a.Cq = _ptr(Bq), _ptr(Cq)
+    else:
+        a.B, a.C, a.bc_dtype = _ptr(Bsrc), _ptr(Csrc), _fdt(Bsrc)
+    a.B_scale, a.C_scale = _ptr(B_scale), _ptr(C_scale)
     a.c_per_token = int(c_per_token)
     a.D, a.corr = _ptr(D), _ptr(corr)
     a.xs_scale, a.xs_per_head = _ptr(xs_scale), int(xs_per_head)
@@ -528,9 +543,22 @@ class SSDi8Layer:
         self.Bq = self.Cq = None
 
     def __call__(self, x, dt, B, C, *, y=None, taps=(), final_state=True, stage_events=None,
-                 path="auto", stream=None):
+                 path="auto", quantize_in_bmm=False, stream=None):
+        """quantize_in_bmm: hand B, C to ChunkBMM unquantized (one launch fewer per tensor, no
+        row-major int8 copies) instead of quantizing them first with ssdi8_quantize_act."""
         Bt, L, H, P = x.shape
         G = B.shape[2]
+        need = workspace_size(dims(Bt, L, H, G))
+        if self.workspace is None or self.workspace.numel() < need:
+            self.workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x.device)
+        if quantize_in_bmm:
+            return ssd_chunk_scan(x, dt, self.A, None, None, self.alpha_B, self.alpha_C,
+                                  self.alpha_Xs, self.alpha_S, self.alpha_CB, D=self.D,
+                                  corr=self.corr, dt_softplus=self.dt_softplus,
+                                  decay_shift=self.decay_shift, shift_round=self.shift_round,
+                                  taps=taps, workspace=self.workspace, y=y,
+                                  final_state=final_state, stage_events=stage_events,
+                                  path=path, B=B, C=C, stream=stream)
         if self.Bq is None or self.Bq.shape != B.shape:
             self.Bq = torch.empty(B.shape, dtype=torch.int8, device=x.device)
             self.Cq = torch.empty(C.shape, dtype=torch.int8, device=x.device)

@@ -370,3 +370,25 @@ def test_mfma_probe_argument_errors(ssdi8):
     assert L.ssdi8_mfma_probe(0, 10, 70000, A16, ctypes.byref(ops), None) == ssdi8.ERR_ARG
     assert L.ssdi8_mfma_probe(0, 10, 4, None, ctypes.byref(ops), None) == ssdi8.ERR_NULL
     assert L.ssdi8_mfma_probe(1, 10, 4, A16 + 2, ctypes.byref(ops), None) == ssdi8.ERR_ALIGN
+
+
+def test_scan_unquantized_bc_arguments(ssdi8):
+    L = ssdi8.lib()
+    d = ssdi8.dims(2, 512, 8, 2)
+    a = ssdi8.ScanArgs()
+    for f in ("x", "dt", "A", "B", "C", "B_scale", "C_scale", "xs_scale", "state_scale",
+              "cb_scale", "y", "workspace"):
+        setattr(a, f, A16)
+    a.x_dtype = a.y_dtype = a.bc_dtype = ssdi8.F16
+    a.decay_shift, a.workspace_bytes = 7, 1 << 40
+    call = lambda: L.ssdi8_ssd_chunk_scan(ctypes.byref(d), ctypes.byref(a), None)
+    a.Bq = A16                        # both forms at once
+    assert call() == ssdi8.ERR_ARG
+    a.Bq = None
+    a.bc_dtype = 5
+    assert call() == ssdi8.ERR_ARG
+    a.bc_dtype = ssdi8.F16
+    a.C = None
+    assert call() == ssdi8.ERR_NULL
+    a.C = A16 + 4
+    assert call() == ssdi8.ERR_ALIGN
