@@ -178,3 +178,27 @@ def test_single_pass_full_size(torch, ssdi8, name):
                            sc["corr"], sc, chunk=cfg.chunk, heads=picks, want=("y64",))
     for (b, h) in picks:
         assert_close(one["y"][b, :, h], ref["slabs"][(b, h)]["y64"], f"y slab ({b},{h})")
+
+
+@pytest.mark.parametrize("batch,nheads,ngroups,nchunks", [(1, 1, 1, 16), (1, 3, 1, 5), (3, 3, 3, 3),
+                                                          (1, 9, 3, 6)])
+def test_single_pass_few_sequences(torch, ssdi8, batch, nheads, ngroups, nchunks):
+    """Fewer sequences than ticket classes (most classes empty, their workgroups draw items from
+    the others) and class sizes that differ by one: every chain still completes, no wait runs
+    out, and the results equal the separate kernels' and the oracle's."""
+    cfg = _small(f"few-{batch}x{nheads}", batch=batch, nheads=nheads, ngroups=ngroups,
+                 seqlen=256 * nchunks, x_outliers=1)
+    say(f"single pass few sequences: B={batch} H={nheads} G={ngroups} chunks={nchunks}")
+    inp = synth.draw(cfg, 1)
+    sc = calibration(cfg)
+    ws = _workspace(torch, ssdi8, cfg)
+    one = run_layer(torch, ssdi8, inp, sc, y_dtype=torch.float32, workspace=ws, path="single")
+    assert _timed_out_waits(ws, cfg) == 0
+    sep = run_layer(torch, ssdi8, inp, sc, y_dtype=torch.float32, path="separate")
+    assert np.array_equal(one["final_state_q"], sep["final_state_q"])
+    rel = np.linalg.norm(one["y"] - sep["y"]) / np.linalg.norm(sep["y"])
+    assert rel <= W_ULP
+    ref = oq.ssdi8_forward(inp["x"], inp["dt_raw"], inp["A"], inp["B"], inp["C"], inp["D"],
+                           sc["corr"], sc, chunk=cfg.chunk, want=("y64", "final_q"))
+    assert np.array_equal(one["final_state_q"], ref["final_q"])
+    assert_close(one["y"], ref["y64"], "y (few sequences)")
