@@ -160,10 +160,10 @@ typedef struct {
      scan1_i32 requested, ChunkState, StatePassing and ChunkScan can run as one single-pass
      kernel in which each chunk waits for the previous chunk of its sequence to hand over the
      int8 entering state (integer results identical; y differs from the separate kernels only by
-     the rounding of ChunkScan's fp32 tables).  0: automatic (the single pass when the sequences
-     have at least 16 chunks and batch * nheads >= 64, where it is the faster one: with fewer
-     chunks the per-chunk hand-off latency is not amortized, with fewer sequences their serial
-     chains bound it); 1: always the separate kernels; 2: the single pass whenever eligible.
+     the rounding of ChunkScan's fp32 tables).  0: automatic (the single pass where it is the
+     faster one, which takes enough concurrent sequences to hide the serial chain of hand-offs:
+     batch * nheads >= 192 with at least 4 chunks, >= 128 with at least 16, or >= 80 with at
+     least 32); 1: always the separate kernels; 2: the single pass whenever eligible.
      With the single pass, events 1-3 of stage_events are recorded back to back before it. */
   int path;
   /* Alternative to Bq / Cq (both NULL then): the unquantized B, C [B,L,G,N] of bc_dtype

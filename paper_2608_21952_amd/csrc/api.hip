@@ -124,9 +124,14 @@ ssdi8_status check_dims(const ssdi8_dims* d) {
 bool single_pass(const ssdi8_dims* d, const ssdi8_scan_args* a) {
   const bool eligible = a->x_dtype == SSDI8_F16 && !a->xs_q && !a->state_i32 && !a->state_q &&
                         !a->decay_q && !a->state_in_q && !a->scan1_i32;
+  if (!eligible) return false;
+  if (a->path != 0) return a->path == 2;
+  // automatic: the single pass hides its chain of nc hand-offs behind enough concurrent
+  // sequences; measured crossover on MI355X (130M-shaped layers, B H sequences of nc chunks):
+  // it wins from 192 sequences at 4 chunks, from 128 at 16 and from 80 at 32 and more
   const int64_t nc = d->chunk > 0 ? d->seqlen / d->chunk : 0;
-  return eligible &&
-         (a->path == 2 || (a->path == 0 && nc >= 16 && d->batch * d->nheads >= 64));
+  const int64_t bh = d->batch * d->nheads;
+  return (bh >= 192 && nc >= 4) || (bh >= 128 && nc >= 16) || (bh >= 80 && nc >= 32);
 }
 
 }  // namespace
@@ -294,6 +299,7 @@ ssdi8_status ssdi8_ssd_chunk_scan(const ssdi8_dims* d, const ssdi8_scan_args* a,
     fs.final_state = a->final_state;
     fs.sync = sync;
     fs.nbh = ld.batch * ld.nheads;
+    fs.nclass = ssdi8::sync_classes(fs.nbh);
     fs.spin_limit = 1 << 16;   // polls of ~1 us: a wait gives up after ~65 ms
     e = ssdi8::launch_chunk_scan_fused(ld, static_cast<const _Float16*>(a->x), a->dt,
                                        a->dt_softplus, a->A, cq, a->C_scale, a->c_per_token, pin,

@@ -32,6 +32,7 @@ namespace ssdi8 {
 namespace {
 
 constexpr int kXTS = kQ * 2 + 16;   // bytes per channel row of x^T (fp16)
+constexpr int kXQS = kQ + 16;       // bytes per channel row of X_q^T (int8, single pass)
 static_assert(kP * kXTS >= kQ * kP * 2, "the fp16 output stage reuses the x^T bytes");
 // A diagonal block whose decay span r_{J-1} - r_J stays below this bound forms its weights as
 // (a_CB dt_i exp(-(cs_i - r_{J-1}))) * exp(cs_j - r_{J-1}) without overflow in fp32.
@@ -124,23 +125,25 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
   const int wv = __builtin_amdgcn_readfirstlane(t >> 6);   // wave-uniform, so block loops are scalar
   int b, c, h;
   if constexpr (kFused) {
-    // Work items in ticket order.  The sequences (b, h) are split into 8 classes of consecutive
-    // sequences; class x hands out its items chunk-major from its own counter sync[x], so the
-    // item a workgroup waits for (same sequence, previous chunk) holds an earlier ticket of the
-    // same counter and is running or done.  A workgroup draws from class blockIdx % 8 (with
-    // round-robin dispatch over the 8 XCDs, a class stays on one XCD, where the heads of one
-    // batch element share the chunk's B_q^T, C_q and CB_q in L2) and, once that class is
-    // exhausted, from the next ones; the grid has as many workgroups as items, so every item
-    // is drawn.
+    // Work items in ticket order.  The sequences (b, h) are split into K classes of consecutive
+    // sequences; class x hands out its items chunk-major from its own counter, so the item a
+    // workgroup waits for (same sequence, previous chunk) holds an earlier ticket of the same
+    // counter and is running or done.  A workgroup draws from class blockIdx % K (with
+    // round-robin dispatch over the 8 XCDs and K a multiple of 8, a class stays on one XCD,
+    // where the heads of one batch element share the chunk's B_q^T, C_q and CB_q in L2) and,
+    // once that class is exhausted, from the next ones; the grid has as many workgroups as
+    // items, so every item is drawn.  K is chosen so that each class holds as many items as
+    // workgroups start on it, and each counter sits on its own cache line: the atomics of a
+    // launch spread over K lines instead of queueing on one.
     if (t == 0) {
-      const int nbh = fs.nbh;
-      const int q = nbh / kSyncClasses, r = nbh - q * kSyncClasses;
+      const int nbh = fs.nbh, K = fs.nclass;
+      const int q = nbh / K, r = nbh - q * K;
       int item = -1;
-      for (int k = 0; k < kSyncClasses && item < 0; ++k) {
-        const int x = (int)((blockIdx.x + k) & (kSyncClasses - 1));
+      for (int k = 0; k < K && item < 0; ++k) {
+        const int x = (int)((blockIdx.x + k) & (K - 1));
         const int chains = q + (x < r ? 1 : 0);
         if (chains <= 0) continue;
-        const int tk = atomicAdd(fs.sync + x, 1);
+        const int tk = atomicAdd(fs.sync + x * kSyncLine, 1);
         if (tk < chains * nc) {
           const int cc = tk / chains;
           item = cc * nbh + x * q + (x < r ? x : r) + (tk - cc * chains);
@@ -168,7 +171,13 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
   const size_t HP = (size_t)H * kP;
   const float aCB = cb_scale[g];
 
-  // ---- x tile loads first (thread: channel pair (p0, p0+1), tokens [32 jb, 32 jb + 32))
+  // ---- loads in the order they are needed (vector loads complete in issue order): dt and the
+  //      per-channel tables first, so that the block scan and the tables wait for them alone
+  //      while the x tile is still in flight
+  float dtv = dt[(tok0 + t) * H + h];
+  const float aSv = t < kP ? state_scale[h * kP + t] : 0.0f;
+  const float crv = (t < kP && corr) ? corr[h * kP + t] : 0.0f;
+  // x tile (thread: channel pair (p0, p0+1), tokens [32 jb, 32 jb + 32))
   const int pp = t & 31, jb = t >> 5, p0 = 2 * pp;
   typename Pair<XT>::raw xr[32];
   {
@@ -177,17 +186,15 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
 #pragma unroll
     for (int r = 0; r < 32; ++r) xr[r] = Pair<XT>::load(xrs, xo, (uint32_t)(r * HP * sizeof(XT)));
   }
-
   // ---- ChunkCumsum (fp64 sums; the factors derived from it only need fp32 accuracy here)
-  float dtv = dt[(tok0 + t) * H + h];
   // the single pass quantizes X_scaled, which needs the fp64 softplus of ChunkState
   if (dt_softplus) dtv = kFused ? softplus_f32(dtv) : softplus_fast(dtv);
   const float dA = dtv * A[h];
   const double cs = block_scan_f64_256((double)dA, s_scan);
   if ((t & 31) == 31) s_r[t >> 5] = cs;
   if (t < kP) {
-    s_aS[t] = state_scale[h * kP + t];
-    s_cr[t] = corr ? corr[h * kP + t] : 0.0f;
+    s_aS[t] = aSv;
+    s_cr[t] = crv;
   }
   __syncthreads();
   // ChunkScan2's tables (the single pass builds them after ChunkState: u shares LDS with LUT)
@@ -216,7 +223,7 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
     if (t == 0) sm.misc[1] = (int)rint(exp(last) * (double)(1 << fs.shift));
   }
   // ---- x^T [p][i] (fp16) in LDS
-  {
+  auto stage_xT = [&]() {
     uint8_t* r0 = s_xT + p0 * kXTS + jb * 64;
     uint8_t* r1 = r0 + kXTS;
 #pragma unroll
@@ -231,6 +238,35 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
       *reinterpret_cast<uint4*>(r0 + 16 * q) = make_uint4(a[0], a[1], a[2], a[3]);
       *reinterpret_cast<uint4*>(r1 + 16 * q) = make_uint4(bb[0], bb[1], bb[2], bb[3]);
     }
+  };
+  if constexpr (!kFused) {
+    stage_xT();
+  } else {
+    // single pass: X_q^T [p][j] (int8, Eq. 7) first, in the bytes x^T takes later: each x
+    // element is quantized once, by the thread that loaded it, with ChunkState's arithmetic
+    __syncthreads();   // LUT_state complete
+    const float ax0 = fs.xs_per_head ? fs.xs_scale[h] : fs.xs_scale[h * kP + p0];
+    const float ax1 = fs.xs_per_head ? ax0 : fs.xs_scale[h * kP + p0 + 1];
+    const float inv0 = 1.0f / ax0, inv1 = 1.0f / ax1;
+    uint32_t w0[8], w1[8];
+#pragma unroll
+    for (int r4 = 0; r4 < 8; ++r4) {
+      int qa[4], qb[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int r = 4 * r4 + i;
+        const float lut = sm.lut[jb * 32 + r];
+        qa[i] = quant_i8(lut * (float)__builtin_bit_cast(_Float16, Pair<XT>::lo(xr[r])), inv0);
+        qb[i] = quant_i8(lut * (float)__builtin_bit_cast(_Float16, Pair<XT>::hi(xr[r])), inv1);
+      }
+      w0[r4] = pack4_i8(qa[0], qa[1], qa[2], qa[3]);
+      w1[r4] = pack4_i8(qb[0], qb[1], qb[2], qb[3]);
+    }
+    uint8_t* q0 = s_xT + p0 * kXQS + jb * 32;
+    *reinterpret_cast<uint4*>(q0) = make_uint4(w0[0], w0[1], w0[2], w0[3]);
+    *reinterpret_cast<uint4*>(q0 + 16) = make_uint4(w0[4], w0[5], w0[6], w0[7]);
+    *reinterpret_cast<uint4*>(q0 + kXQS) = make_uint4(w1[0], w1[1], w1[2], w1[3]);
+    *reinterpret_cast<uint4*>(q0 + kXQS + 16) = make_uint4(w1[4], w1[5], w1[6], w1[7]);
   }
   __syncthreads();
 
@@ -239,11 +275,10 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
   const int prow = mt * 32 + (lane & 31);
   uint32_t sq[2][4];   // S_q of the two tiles, byte r of word r / 4 = MFMA result row r
   if constexpr (kFused) {
-    // ---- ChunkState (Eq. 7-8), transposed: S32^T = B_q^T X_q with X_q formed from the x^T
-    //      bytes in LDS.  Lane -> channel p = 32 mt + l % 32 and, per tile, the 16 state rows n
-    //      of the permuted kslice order (frag.hpp), which is where the MFMA leaves them.
+    // ---- ChunkState (Eq. 7-8), transposed: S32^T = B_q^T X_q with the X_q^T fragments staged
+    //      above.  Lane -> channel p = 32 mt + l % 32 and, per tile, the 16 state rows n of the
+    //      permuted kslice order (frag.hpp), which is where the MFMA leaves them.
     const float axs = fs.xs_per_head ? fs.xs_scale[h] : fs.xs_scale[h * kP + prow];
-    const float inv = 1.0f / axs;
     const float msp =
         (float)(((double)axs * (double)fs.B_scale[g]) / (double)state_scale[h * kP + prow]);
     {
@@ -251,32 +286,14 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
           buffer_rsrc(fs.bqT + (((size_t)b * nc + c) * G + g) * (size_t)kN * kQ);
       const uint32_t l16 = lane * 16;
       v16i s0 = {}, s1 = {};
+      const uint8_t* arow = s_xT + prow * kXQS + 16 * hf;
 #pragma unroll
       for (int ks = 0; ks < kQ / 32; ++ks) {
         const v4i bf0 = __builtin_bit_cast(
             v4i, buf_load16(brs, l16, (uint32_t)((ntb * (kQ / 32) + ks) * 1024)));
         const v4i bf1 = __builtin_bit_cast(
             v4i, buf_load16(brs, l16, (uint32_t)(((ntb + 1) * (kQ / 32) + ks) * 1024)));
-        const int j0 = ks * 32 + 16 * hf;
-        const uint4 xa = *reinterpret_cast<const uint4*>(s_xT + prow * kXTS + j0 * 2);
-        const uint4 xb = *reinterpret_cast<const uint4*>(s_xT + prow * kXTS + j0 * 2 + 16);
-        const uint32_t xw[8] = {xa.x, xa.y, xa.z, xa.w, xb.x, xb.y, xb.z, xb.w};
-        uint32_t qw[4];
-#pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4) {
-          const float4 l4 = *reinterpret_cast<const float4*>(sm.lut + j0 + 4 * q4);
-          const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
-          int qv[4];
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const uint32_t wd = xw[2 * q4 + (e >> 1)];
-            const float xv = (float)__builtin_bit_cast(
-                _Float16, (uint16_t)((e & 1) ? (wd >> 16) : (wd & 0xffffu)));
-            qv[e] = quant_i8(lv[e] * xv, inv);
-          }
-          qw[q4] = pack4_i8(qv[0], qv[1], qv[2], qv[3]);
-        }
-        const v4i a = {(int)qw[0], (int)qw[1], (int)qw[2], (int)qw[3]};
+        const v4i a = *reinterpret_cast<const v4i*>(arow + ks * 32);
         s0 = __builtin_amdgcn_mfma_i32_32x32x32_i8(bf0, a, s0, 0, 0, 0);
         s1 = __builtin_amdgcn_mfma_i32_32x32x32_i8(bf1, a, s1, 0, 0, 0);
       }
@@ -289,7 +306,10 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
                              requant_i8(s1[4 * w4 + 2], msp), requant_i8(s1[4 * w4 + 3], msp));
       }
     }
-    __syncthreads();   // LUT no longer read: its bytes become ChunkScan2's u table
+    // X_q^T and LUT_state no longer read: x^T and ChunkScan2's tables (u over LUT) take their
+    // bytes
+    __syncthreads();
+    stage_xT();
     scan_tables();
     __syncthreads();
   }
@@ -312,7 +332,7 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
         }
         __builtin_amdgcn_s_sleep(2);
       }
-      if (!ok) atomicAdd(fs.sync + kSyncClasses, 1);
+      if (!ok) atomicAdd(fs.sync + kSyncWait, 1);
     }
     __syncthreads();
     {
@@ -450,13 +470,18 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
       auto qbyte = [](uint32_t ub0, uint32_t ub1, int e) {
         return (float)(((e < 4 ? ub0 : ub1) >> (8 * (e & 3))) & 0xffu);
       };
-      uint4 cur = buf_load16(cbrs, lane16, cbrow);
-      // off-diagonal blocks it < jt: straight-line body, CB_q of block it+1 (the diagonal block
-      // after the last one) in flight meanwhile
-      for (int it = 0; it < jt; ++it) {
-        const uint4 nx = buf_load16(cbrs, lane16, cbrow + (it + 1) * 1024);
-        // keep the prefetch at the top of the body (left alone, the scheduler sinks it to the
-        // end, and the next iteration waits for the full L2 latency)
+      // CB_q fragments in a ring of three register sets: block it is built while blocks it+1 and
+      // it+2 are in flight.  The off-diagonal steps are written out so that every slot stays a
+      // fixed register set (a copy between slots would wait for the load in flight), and every
+      // load is unconditional, its block index clamped to the row's last block jt (a branch
+      // around a load makes the wait after it a full drain).
+      uint4 r0 = buf_load16(cbrs, lane16, cbrow);
+      uint4 r1 = buf_load16(cbrs, lane16, cbrow + (jt < 1 ? jt : 1) * 1024);
+      uint4 r2;
+      // off-diagonal block it < jt from slot cur; block min(it + 2, jt) into dst
+      auto off_block = [&](const int it, const uint4& cur, uint4& dst) {
+        dst = buf_load16(cbrs, lane16, cbrow + (it + 2 < jt ? it + 2 : jt) * 1024);
+        // keep the prefetch at the top of the body
         __builtin_amdgcn_sched_barrier(0);
         // row factor: exp(cs_j - r_{J-1}) exp(r_{J-1} - r_I)
         const float vj = ej * s_R[jt - 1][it];
@@ -473,8 +498,28 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
           }
           mfma_block(wv, i0);
         }
-        cur = nx;
+      };
+      if (jt > 0) {
+        off_block(0, r0, r2);
+        if (jt > 1) {
+          off_block(1, r1, r0);
+          if (jt > 2) {
+            off_block(2, r2, r1);
+            if (jt > 3) {
+              off_block(3, r0, r2);
+              if (jt > 4) {
+                off_block(4, r1, r0);
+                if (jt > 5) {
+                  off_block(5, r2, r1);
+                  if (jt > 6) off_block(6, r0, r2);
+                }
+              }
+            }
+          }
+        }
       }
+      const int js = jt % 3;
+      const uint4 cur = js == 0 ? r0 : (js == 1 ? r1 : r2);
       // the C_q fragments of ChunkScan1, in flight during the diagonal block
       {
         const uint32_t crow = jt * (kN / 32) * 1024;

@@ -59,11 +59,22 @@ hipError_t launch_chunk_scan(const LayerDims& d, const void* x, int x_dtype, con
 // Single pass of ChunkState, StatePassing and ChunkScan (fp16 x): one workgroup per (b, c, h)
 // in ticket order; each computes its chunk's S_q, waits for the previous chunk of its sequence
 // to publish P_in[c] (pin slot c, permuted kslice order, as C_q), publishes P_in[c+1] (slot
-// c + 1, or the final states) and runs ChunkScan1/2 with x still in LDS.  sync: [0, 8) the
-// ticket counters of the 8 sequence classes, [8] count of waits that ran out,
-// [16 + (b H + h) nc + c] flag "slot c + 1 published"; cleared beforehand (ChunkBMM).
-constexpr int kSyncClasses = 8;
-constexpr int kSyncFlags = 16;
+// c + 1, or the final states) and runs ChunkScan1/2 with x still in LDS.  sync (int words,
+// cleared beforehand by ChunkBMM): the ticket counter of sequence class x at x * kSyncLine (one
+// 128-byte line each, so that the classes' atomics do not serialize on one line), the count of
+// waits that ran out at kSyncWait, and from kSyncFlags + (b H + h) nc + c the flag "slot c + 1
+// published".
+constexpr int kSyncLine = 32;
+constexpr int kSyncMaxClasses = 64;
+constexpr int kSyncWait = kSyncMaxClasses * kSyncLine;
+constexpr int kSyncFlags = kSyncWait + kSyncLine;
+// Sequence classes of a launch: the largest of 64, 32, 16, 8 that divides the B H sequences
+// (every class then holds as many items as workgroups draw from it first), else 8.
+inline int sync_classes(int nbh) {
+  for (int k = kSyncMaxClasses; k > 8; k >>= 1)
+    if (nbh % k == 0) return k;
+  return 8;
+}
 struct FusedState {
   const int8_t* bqT = nullptr;
   const float* B_scale = nullptr;
@@ -76,6 +87,7 @@ struct FusedState {
   float* final_state = nullptr;
   int* sync = nullptr;
   int nbh = 0;
+  int nclass = 8;       // sync_classes(nbh)
   int spin_limit = 0;
 };
 hipError_t launch_chunk_scan_fused(const LayerDims& d, const _Float16* x, const float* dt,

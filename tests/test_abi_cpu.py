@@ -173,9 +173,11 @@ def test_workspace_size(ssdi8):
     d = ssdi8.dims(4, 4096, 80, 1)
     B, L, H, P, G, N, Q = 4, 4096, 80, 64, 1, 128, 256
     c = L // Q
-    # B_q^T and C_q copies, S_q and P_in, the 36 causal 32x32 blocks of CB_q, Q(Decay)
+    # B_q^T and C_q copies, S_q and P_in, the 36 causal 32x32 blocks of CB_q, Q(Decay), and the
+    # single-pass hand-off words: 64 ticket counters on lines of 32 words, the line of the wait
+    # counter, one flag per item
     need = (2 * B * L * G * N + 2 * B * c * H * P * N + B * c * G * 36 * 32 * 32 + B * H * c * 2
-            + 4 * (16 + B * H * c))     # + the single-pass ticket counters, wait counter, flags
+            + 4 * (64 * 32 + 32 + B * H * c))
     ws = ssdi8.workspace_size(d)
     assert need <= ws <= need + 7 * 256
     assert ssdi8.workspace_size(ssdi8.dims(1, 300, 4, 1)) == 0          # L % chunk
@@ -335,10 +337,16 @@ def test_single_pass_selection(ssdi8):
     import torch
     f16, f32 = torch.float16, torch.float32
     use = lambda dd, *a, **k: ssdi8.uses_single_pass(dd, *a, **k)
-    assert not use(ssdi8.dims(8, 2048, 24, 1), f16)            # 8 chunks: separate
+    assert use(ssdi8.dims(8, 2048, 24, 1), f16)                # 192 sequences of 8 chunks
+    assert not use(ssdi8.dims(4, 2048, 24, 1), f16)            # 96 sequences of 8 chunks
+    assert not use(ssdi8.dims(8, 512, 24, 1), f16)             # 2 chunks
+    assert use(ssdi8.dims(4, 4096, 32, 1), f16)                # 128 sequences of 16 chunks
+    assert not use(ssdi8.dims(4, 2048, 32, 1), f16)            # 128 sequences of 8 chunks
     assert use(ssdi8.dims(4, 4096, 80, 1), f16)                # 16 chunks, 320 sequences
     assert use(ssdi8.dims(2, 8192, 128, 8), f16)
     assert use(ssdi8.dims(1, 65536, 80, 1), f16)               # 80 sequences of 256 chunks
+    assert use(ssdi8.dims(1, 16384, 80, 1), f16)               # 80 sequences of 64 chunks
+    assert not use(ssdi8.dims(1, 4096, 96, 1), f16)            # 96 sequences of 16 chunks
     assert not use(ssdi8.dims(1, 65536, 48, 1), f16)           # 48 sequences: chain-bound
     assert use(ssdi8.dims(8, 2048, 24, 1), f16, "single")
     assert not use(ssdi8.dims(4, 4096, 80, 1), f16, "separate")

@@ -40,14 +40,20 @@ def _workspace(torch, ssdi8, cfg):
     return torch.empty(ssdi8.workspace_size(d), dtype=torch.uint8, device="cuda")
 
 
+# hand-off words: a ticket counter per 128-byte line for up to 64 sequence classes, the count of
+# waits that ran out on the next line, then the flags
+SYNC_LINE, SYNC_CLASSES = 32, 64
+SYNC_WAIT = SYNC_CLASSES * SYNC_LINE
+SYNC_FLAGS = SYNC_WAIT + SYNC_LINE
+
+
 def _timed_out_waits(ws, cfg):
-    """The hand-off words are the last region of the workspace: [8 ticket counters, waits that
-    ran out, 7 spare, flags ...], padded to 256 bytes."""
+    """The hand-off words are the last region of the workspace, padded to 256 bytes."""
     nc = cfg.seqlen // cfg.chunk
-    n = 16 + cfg.batch * cfg.nheads * nc
+    n = SYNC_FLAGS + cfg.batch * cfg.nheads * nc
     off = ws.numel() - ((4 * n + 255) // 256) * 256
-    words = ws[off:off + 64].cpu().numpy().view(np.int32)
-    return int(words[8])
+    words = ws[off:off + 4 * (SYNC_WAIT + 1)].cpu().numpy().view(np.int32)
+    return int(words[SYNC_WAIT])
 
 
 def _small(name, **kw):
