@@ -315,8 +315,8 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
   }
 
   // ---- single pass, StatePassing (Eq. 9) for this chunk: wait until the previous chunk of the
-  //      sequence has published P_in[c] (bounded: a wait
-  //      that runs out is counted in sync[8] and the kernel still finishes), then
+  //      sequence has published P_in[c] (bounded: a wait that runs out is counted in the
+  //      wait counter sync[kSyncWait] and the kernel still finishes), then
   //      P_in[c+1] = clamp(S_q + ((q_d P_in[c] + r) >> k)), published with agent-coherent
   //      stores before the flag.  Every lane updates its own 32 state bytes in registers.
   auto hand_off = [&]() {
