@@ -125,28 +125,30 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
   const int wv = __builtin_amdgcn_readfirstlane(t >> 6);   // wave-uniform, so block loops are scalar
   int b, c, h;
   if constexpr (kFused) {
-    // Work items in ticket order.  The sequences (b, h) are split into K classes of consecutive
-    // sequences; class x hands out its items chunk-major from its own counter, so the item a
-    // workgroup waits for (same sequence, previous chunk) holds an earlier ticket of the same
-    // counter and is running or done.  A workgroup draws from class blockIdx % K (with
-    // round-robin dispatch over the 8 XCDs and K a multiple of 8, a class stays on one XCD,
-    // where the heads of one batch element share the chunk's B_q^T, C_q and CB_q in L2) and,
+    // Work items in ticket order.  The sequences (b, h) are split into K blocks of consecutive
+    // sequences, one per class; class x hands out its items chunk-major from its own counter, so
+    // the item a workgroup waits for (same sequence, previous chunk) holds an earlier ticket of
+    // the same counter and is running or done.  A workgroup draws from class blockIdx % K and,
     // once that class is exhausted, from the next ones; the grid has as many workgroups as
-    // items, so every item is drawn.  K is chosen so that each class holds as many items as
-    // workgroups start on it, and each counter sits on its own cache line: the atomics of a
-    // launch spread over K lines instead of queueing on one.
+    // items, so every item is drawn.  K (a multiple of 8) is chosen so that each class holds as
+    // many items as workgroups start on it, and each counter sits on its own cache line: the
+    // atomics of a launch spread over K lines instead of queueing on one.  With round-robin
+    // dispatch over the 8 XCDs, class x runs on XCD x % 8, and the K / 8 classes of one XCD take
+    // consecutive sequence blocks, so that the heads of one batch element (which share the
+    // chunk's B_q^T, C_q and CB_q) meet in as few L2 caches as possible.
     if (t == 0) {
       const int nbh = fs.nbh, K = fs.nclass;
       const int q = nbh / K, r = nbh - q * K;
       int item = -1;
       for (int k = 0; k < K && item < 0; ++k) {
         const int x = (int)((blockIdx.x + k) & (K - 1));
-        const int chains = q + (x < r ? 1 : 0);
+        const int sb = (x & 7) * (K >> 3) + (x >> 3);   // sequence block of class x
+        const int chains = q + (sb < r ? 1 : 0);
         if (chains <= 0) continue;
         const int tk = atomicAdd(fs.sync + x * kSyncLine, 1);
         if (tk < chains * nc) {
           const int cc = tk / chains;
-          item = cc * nbh + x * q + (x < r ? x : r) + (tk - cc * chains);
+          item = cc * nbh + sb * q + (sb < r ? sb : r) + (tk - cc * chains);
         }
       }
       sm.misc[0] = item;
