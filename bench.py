@@ -28,6 +28,22 @@ MODULES = ("chunk_bmm", "chunk_state", "state_pass", "chunk_scan")
 # the single pass (fp16 x): ChunkState + StatePassing + ChunkScan in one kernel after ChunkBMM
 SINGLE = ("chunk_bmm", "single_pass")
 SOURCE = {"single_pass": "chunk_scan"}      # kernel -> source file of its HIP code
+# headers every kernel source compiles in: a change to them is a change to the kernel
+KERNEL_HEADERS = ("common.hpp", "frag.hpp", "launch.hpp")
+
+
+def kernel_source_sha256(kernel: str):
+    """sha256 over the kernel's .hip source followed by the shared headers (None if missing)."""
+    import hashlib
+    csrc = os.path.join(ROOT, "paper_2608_21952_amd", "csrc")
+    h = hashlib.sha256()
+    for name in (f"{SOURCE.get(kernel, kernel)}.hip",) + KERNEL_HEADERS:
+        path = os.path.join(csrc, name)
+        if not os.path.exists(path):
+            return None
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
 
 
 def algorithmic_bytes(cfg, quant_in_bmm=False):
@@ -80,17 +96,16 @@ def layer_min_bytes(cfg):
 def measured_traffic(kernel: str, workload: str):
     """HBM bytes per launch of `kernel` from the committed rocprofv3 FETCH_SIZE / WRITE_SIZE
     summary (each counter scaled by what it reads for a plain copy of known size), or None when
-    there is none or the kernel's source changed since the counters were taken."""
-    import hashlib
+    there is none or the kernel's source or a shared header changed since the counters were
+    taken."""
     path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload}.json")
-    src = os.path.join(ROOT, "paper_2608_21952_amd", "csrc", f"{SOURCE.get(kernel, kernel)}.hip")
-    if not os.path.exists(path) or not os.path.exists(src):
+    digest = kernel_source_sha256(kernel)
+    if not os.path.exists(path) or digest is None:
         return None
     with open(path) as f:
         rec = json.load(f)
-    with open(src, "rb") as f:
-        if hashlib.sha256(f.read()).hexdigest() != rec.get("source_sha256"):
-            return None
+    if digest != rec.get("source_sha256"):
+        return None
     return rec.get("bytes_per_launch")
 
 

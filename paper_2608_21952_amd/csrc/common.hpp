@@ -77,17 +77,33 @@ __device__ __forceinline__ int xcd_remap(int bid, int nwg) {
   return (xcd < r) ? xcd * (q + 1) + idx : r * (q + 1) + (xcd - r) * q + idx;
 }
 
+// v + the value of the lane that DPP control kCtrl selects (0 where there is none or where the
+// lane's row is outside kRowMask): one 64-lane data-parallel-primitive move per 32-bit half.
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ double dpp_add_f64(double v) {
+  const uint64_t u = __builtin_bit_cast(uint64_t, v);
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)u, kCtrl, kRowMask,
+                                                            0xf, false);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(u >> 32), kCtrl,
+                                                            kRowMask, 0xf, false);
+  return v + __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
+}
+
 // Inclusive prefix sum over the 256 threads of a block in fp64.  The in-chunk sums of fp32
 // decay increments are exact in fp64 (the terms of one chunk span few binades), so the tree
-// order used here gives the same values as a sequential sum.  `scratch` holds 4 doubles.
+// order used here gives the same values as a sequential sum.  Within a wave: shifts by 1, 2, 4,
+// 8 lanes inside each row of 16 (row_shr), then the last lane of row 0 / 2 into rows 1 / 3
+// (row_bcast:15) and the last lane of row 1 into rows 2 and 3 (row_bcast:31), all in registers;
+// across the four waves through `scratch` (4 doubles).
 __device__ __forceinline__ double block_scan_f64_256(double v, double* scratch) {
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    double t = __shfl_up(v, off, 64);
-    if (lane >= off) v += t;
-  }
+  v = dpp_add_f64<0x111, 0xf>(v);
+  v = dpp_add_f64<0x112, 0xf>(v);
+  v = dpp_add_f64<0x114, 0xf>(v);
+  v = dpp_add_f64<0x118, 0xf>(v);
+  v = dpp_add_f64<0x142, 0xa>(v);
+  v = dpp_add_f64<0x143, 0xc>(v);
   if (lane == 63) scratch[w] = v;
   __syncthreads();
   double pre = 0.0;
