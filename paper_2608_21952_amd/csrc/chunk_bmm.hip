@@ -53,15 +53,15 @@ template <> struct Row16<_Float16> {
     uint32_t o[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      int q[4];
+      uint32_t q[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const uint32_t wd = w[2 * i + (e >> 1)];
-        q[e] = quant_i8((float)__builtin_bit_cast(_Float16, (uint16_t)((e & 1) ? (wd >> 16)
-                                                                                : (wd & 0xffffu))),
-                        inv);
+        q[e] = quant_bits((float)__builtin_bit_cast(_Float16, (uint16_t)((e & 1) ? (wd >> 16)
+                                                                                  : (wd & 0xffffu))),
+                          inv);
       }
-      o[i] = pack4_i8(q[0], q[1], q[2], q[3]);
+      o[i] = pack_lo4(q[0], q[1], q[2], q[3]);
     }
     return make_uint4(o[0], o[1], o[2], o[3]);
   }
@@ -72,8 +72,8 @@ template <> struct Row16<float> {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const float4 f = reinterpret_cast<const float4*>(p)[i];
-      o[i] = pack4_i8(quant_i8(f.x, inv), quant_i8(f.y, inv), quant_i8(f.z, inv),
-                      quant_i8(f.w, inv));
+      o[i] = pack_lo4(quant_bits(f.x, inv), quant_bits(f.y, inv), quant_bits(f.z, inv),
+                      quant_bits(f.w, inv));
     }
     return make_uint4(o[0], o[1], o[2], o[3]);
   }

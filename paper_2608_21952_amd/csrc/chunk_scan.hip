@@ -253,16 +253,16 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
     uint32_t w0[8], w1[8];
 #pragma unroll
     for (int r4 = 0; r4 < 8; ++r4) {
-      int qa[4], qb[4];
+      uint32_t qa[4], qb[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int r = 4 * r4 + i;
         const float lut = sm.lut[jb * 32 + r];
-        qa[i] = quant_i8(lut * (float)__builtin_bit_cast(_Float16, Pair<XT>::lo(xr[r])), inv0);
-        qb[i] = quant_i8(lut * (float)__builtin_bit_cast(_Float16, Pair<XT>::hi(xr[r])), inv1);
+        qa[i] = quant_bits(lut * (float)__builtin_bit_cast(_Float16, Pair<XT>::lo(xr[r])), inv0);
+        qb[i] = quant_bits(lut * (float)__builtin_bit_cast(_Float16, Pair<XT>::hi(xr[r])), inv1);
       }
-      w0[r4] = pack4_i8(qa[0], qa[1], qa[2], qa[3]);
-      w1[r4] = pack4_i8(qb[0], qb[1], qb[2], qb[3]);
+      w0[r4] = pack_lo4(qa[0], qa[1], qa[2], qa[3]);
+      w1[r4] = pack_lo4(qb[0], qb[1], qb[2], qb[3]);
     }
     uint8_t* q0 = s_xT + p0 * kXQS + jb * 32;
     *reinterpret_cast<uint4*>(q0) = make_uint4(w0[0], w0[1], w0[2], w0[3]);
@@ -302,10 +302,10 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
       // S_q = requant(S32, m_S[p]) (Eq. 8), one multiplier per lane
 #pragma unroll
       for (int w4 = 0; w4 < 4; ++w4) {
-        sq[0][w4] = pack4_i8(requant_i8(s0[4 * w4], msp), requant_i8(s0[4 * w4 + 1], msp),
-                             requant_i8(s0[4 * w4 + 2], msp), requant_i8(s0[4 * w4 + 3], msp));
-        sq[1][w4] = pack4_i8(requant_i8(s1[4 * w4], msp), requant_i8(s1[4 * w4 + 1], msp),
-                             requant_i8(s1[4 * w4 + 2], msp), requant_i8(s1[4 * w4 + 3], msp));
+        sq[0][w4] = pack_lo4(requant_bits(s0[4 * w4], msp), requant_bits(s0[4 * w4 + 1], msp),
+                             requant_bits(s0[4 * w4 + 2], msp), requant_bits(s0[4 * w4 + 3], msp));
+        sq[1][w4] = pack_lo4(requant_bits(s1[4 * w4], msp), requant_bits(s1[4 * w4 + 1], msp),
+                             requant_bits(s1[4 * w4 + 2], msp), requant_bits(s1[4 * w4 + 3], msp));
       }
     }
     // X_q^T and LUT_state no longer read: x^T and ChunkScan2's tables (u over LUT) take their

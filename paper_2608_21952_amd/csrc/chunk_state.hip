@@ -110,16 +110,16 @@ __global__ __launch_bounds__(256, sizeof(XT) == 2 ? 6 : 4) void chunk_state_kern
     uint32_t w0[8], w1[8];
 #pragma unroll
     for (int r4 = 0; r4 < 8; ++r4) {
-      int qa[4], qb[4];
+      uint32_t qa[4], qb[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int r = 4 * r4 + i;
         const float lut = s_lut[jb * 32 + r];
-        qa[i] = quant_i8(lut * Pair<XT>::lo(xr[r]), inv0);
-        qb[i] = quant_i8(lut * Pair<XT>::hi(xr[r]), inv1);
+        qa[i] = quant_bits(lut * Pair<XT>::lo(xr[r]), inv0);
+        qb[i] = quant_bits(lut * Pair<XT>::hi(xr[r]), inv1);
       }
-      w0[r4] = pack4_i8(qa[0], qa[1], qa[2], qa[3]);
-      w1[r4] = pack4_i8(qb[0], qb[1], qb[2], qb[3]);
+      w0[r4] = pack_lo4(qa[0], qa[1], qa[2], qa[3]);
+      w1[r4] = pack_lo4(qb[0], qb[1], qb[2], qb[3]);
     }
     int8_t* r0 = s_xq + p0 * kXS + jb * 32;
     int8_t* r1 = r0 + kXS;

@@ -47,17 +47,35 @@ __device__ __forceinline__ void buf_store16(uint4 d, __amdgpu_buffer_rsrc_t r, u
 }
 
 // Symmetric int8 quantization of an fp32 value with a precomputed inverse step:
-// clamp(rne(v * inv), -127, 127).  One IEEE fp32 product, round-half-even to integer.
+// clamp(rne(v * inv), -127, 127).  One IEEE fp32 product, round-half-even to integer.  Formed
+// as rne(clamp(p)), which is the same value (rne is monotonic and fixes +-127), with the
+// rounding done by adding 1.5 * 2^23: every sum lies in [2^23, 2^24), where fp32 steps by 1,
+// so the addition rounds c to an integer, ties to even, and the sum's bit pattern is
+// 0x4B400000 + c; its low byte is c as a two's-complement int8.  A NaN product clamps to -127
+// either way.
+// quant_bits returns that bit pattern (the code in its low byte), for packing; quant_i8 the code.
+__device__ __forceinline__ uint32_t quant_bits(float v, float inv) {
+  const float c = __builtin_fminf(__builtin_fmaxf(v * inv, -127.0f), 127.0f);
+  return __builtin_bit_cast(uint32_t, c + 12582912.0f);
+}
 __device__ __forceinline__ int quant_i8(float v, float inv) {
-  float p = v * inv;
-  float r = __builtin_rintf(p);
-  r = __builtin_fminf(__builtin_fmaxf(r, -127.0f), 127.0f);
-  return (int)r;
+  return (int)quant_bits(v, inv) - 0x4B400000;
 }
 
 // INT32 accumulator -> int8 with an fp32 multiplier: clamp(rne(fl32(acc) * m)).
+__device__ __forceinline__ uint32_t requant_bits(int acc, float m) {
+  return quant_bits((float)acc, m);
+}
 __device__ __forceinline__ int requant_i8(int acc, float m) {
   return quant_i8((float)acc, m);
+}
+
+// The low bytes of four words in one dword (byte i = low byte of w_i): two byte permutes and a
+// shift-or.
+__device__ __forceinline__ uint32_t pack_lo4(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3) {
+  const uint32_t lo = __builtin_amdgcn_perm(w1, w0, 0x0c0c0400u);
+  const uint32_t hi = __builtin_amdgcn_perm(w3, w2, 0x0c0c0400u);
+  return lo | (hi << 16);
 }
 
 // softplus in fp64 with the usual threshold, rounded once to fp32.

@@ -53,22 +53,22 @@ __global__ __launch_bounds__(256) void quant_static_vec16(const T* __restrict__ 
       }
     }
     const I row = v / rowvecs;
-    int q[16];
+    uint32_t q[16];
     if (gran == 2) {
       const I c0 = (row % k) * m + (v - row * rowvecs) * 16;   // channel of element 0
 #pragma unroll
-      for (int i = 0; i < 16; ++i) q[i] = quant_i8(x[i], 1.0f / scale[c0 + i]);
+      for (int i = 0; i < 16; ++i) q[i] = quant_bits(x[i], 1.0f / scale[c0 + i]);
     } else {
       const I gi = gran == 0 ? 0 : (gran == 1 ? row % k : row);
       const float inv = 1.0f / scale[gi];
 #pragma unroll
-      for (int i = 0; i < 16; ++i) q[i] = quant_i8(x[i], inv);
+      for (int i = 0; i < 16; ++i) q[i] = quant_bits(x[i], inv);
     }
     uint4 o;
-    o.x = pack4_i8(q[0], q[1], q[2], q[3]);
-    o.y = pack4_i8(q[4], q[5], q[6], q[7]);
-    o.z = pack4_i8(q[8], q[9], q[10], q[11]);
-    o.w = pack4_i8(q[12], q[13], q[14], q[15]);
+    o.x = pack_lo4(q[0], q[1], q[2], q[3]);
+    o.y = pack_lo4(q[4], q[5], q[6], q[7]);
+    o.z = pack_lo4(q[8], q[9], q[10], q[11]);
+    o.w = pack_lo4(q[12], q[13], q[14], q[15]);
     *reinterpret_cast<uint4*>(dst + e0) = o;
   }
 }
@@ -95,14 +95,14 @@ __global__ __launch_bounds__(256) void quant_static_h8(const _Float16* __restric
     if (unit >= nunit) break;
     const uint32_t row = unit / rowunits;
     const uint32_t w[4] = {raw[u].x, raw[u].y, raw[u].z, raw[u].w};
-    int q[8];
+    uint32_t q[8];
     if (gran == 2) {
       const uint32_t c0 = (row % k) * m + (unit - row * rowunits) * 8;
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
         const float x = (float)__builtin_bit_cast(
             _Float16, (uint16_t)((i & 1) ? (w[i >> 1] >> 16) : (w[i >> 1] & 0xffffu)));
-        q[i] = quant_i8(x, 1.0f / scale[c0 + i]);
+        q[i] = quant_bits(x, 1.0f / scale[c0 + i]);
       }
     } else {
       const uint32_t gi = gran == 0 ? 0u : (gran == 1 ? row % k : row);
@@ -111,11 +111,11 @@ __global__ __launch_bounds__(256) void quant_static_h8(const _Float16* __restric
       for (int i = 0; i < 8; ++i) {
         const float x = (float)__builtin_bit_cast(
             _Float16, (uint16_t)((i & 1) ? (w[i >> 1] >> 16) : (w[i >> 1] & 0xffffu)));
-        q[i] = quant_i8(x, inv);
+        q[i] = quant_bits(x, inv);
       }
     }
     reinterpret_cast<uint2*>(dst)[unit] =
-        make_uint2(pack4_i8(q[0], q[1], q[2], q[3]), pack4_i8(q[4], q[5], q[6], q[7]));
+        make_uint2(pack_lo4(q[0], q[1], q[2], q[3]), pack_lo4(q[4], q[5], q[6], q[7]));
   }
 }
 
