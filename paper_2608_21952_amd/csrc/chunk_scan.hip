@@ -72,12 +72,6 @@ __device__ __forceinline__ float softplus_fast(float v) {
   return v > 20.0f ? v : lp;
 }
 
-// One INT8 StatePassing step of an element (Eq. 9): clamp(S_q + ((q_d P_in + r) >> k)).
-__device__ __forceinline__ int pass_step(int s, int add, int q, int shift, int radd) {
-  const int v = add + ((q * s + radd) >> shift);
-  return v < -kQMax ? -kQMax : (v > kQMax ? kQMax : v);
-}
-
 template <typename XT, typename YT, bool kFused>
 __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
     const XT* __restrict__ x, const float* __restrict__ dt, const float* __restrict__ A,

@@ -70,6 +70,14 @@ __device__ __forceinline__ int requant_i8(int acc, float m) {
   return quant_i8((float)acc, m);
 }
 
+// One INT8 StatePassing step of an element (Eq. 9): clamp(S_q + ((q_d P_in + r) >> k), +-127)
+// with an arithmetic shift.  q_d is an int16 and P_in an int8, so the product is exact in the
+// full-rate 24-bit multiply (a plain int product compiles to the quarter-rate 32-bit one).
+__device__ __forceinline__ int pass_step(int s, int add, int q, int shift, int radd) {
+  const int v = add + ((__mul24(q, s) + radd) >> shift);
+  return v < -kQMax ? -kQMax : (v > kQMax ? kQMax : v);
+}
+
 // The low bytes of four words in one dword (byte i = low byte of w_i): two byte permutes and a
 // shift-or.
 __device__ __forceinline__ uint32_t pack_lo4(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3) {

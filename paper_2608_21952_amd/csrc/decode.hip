@@ -77,11 +77,10 @@ __global__ __launch_bounds__(256) void decode_kernel(
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int bq = sext8(bw[d], e), cq = sext8(cw[d], e), s = sext8(sw[d], e);
-        y1 += cq * s;                       // ChunkScan1 on the entering state
-        cb += cq * bq;                      // C.B^T of the token with itself
-        const int sq = requant_i8(xq * bq, ms);
-        const int v = sq + ((qd * s + radd) >> shift);
-        o[e] = v < -kQMax ? -kQMax : (v > kQMax ? kQMax : v);
+        y1 += __mul24(cq, s);               // ChunkScan1 on the entering state
+        cb += __mul24(cq, bq);              // C.B^T of the token with itself
+        const int sq = requant_i8(__mul24(xq, bq), ms);
+        o[e] = pass_step(s, sq, qd, shift, radd);
         nf[16 * half + 4 * d + e] = o[e];
       }
       ow[d] = pack4_i8(o[0], o[1], o[2], o[3]);

@@ -17,11 +17,6 @@ namespace ssdi8 {
 
 namespace {
 
-__device__ __forceinline__ int step_state(int s, int add, int q, int shift, int radd) {
-  const int v = add + ((q * s + radd) >> shift);
-  return v < -kQMax ? -kQMax : (v > kQMax ? kQMax : v);
-}
-
 // kW dwords (4 kW int8 elements) per thread; kFragK = 0: S_q / P_in row-major, kFragK = N:
 // kslice order with K = N.
 template <int kW> struct Vec;
@@ -101,7 +96,7 @@ __global__ __launch_bounds__(256) void state_pass_kernel(
         if (pin_tap) Vec<kW>::store(pin_tap + base - off + roff + (size_t)(c0 + k) * cstride, o);
 #pragma unroll
         for (int i = 0; i < kE; ++i)
-          st[i] = step_state(st[i], sext8(v[buf][k][i >> 2], i & 3), q[buf][k], shift, radd);
+          st[i] = pass_step(st[i], sext8(v[buf][k][i >> 2], i & 3), q[buf][k], shift, radd);
       }
     }
   };
