@@ -115,8 +115,9 @@ __global__ __launch_bounds__(256, sizeof(XT) == 2 ? 6 : 4) void chunk_state_kern
       for (int i = 0; i < 4; ++i) {
         const int r = 4 * r4 + i;
         const float lut = s_lut[jb * 32 + r];
-        qa[i] = quant_bits(lut * Pair<XT>::lo(xr[r]), inv0);
-        qb[i] = quant_bits(lut * Pair<XT>::hi(xr[r]), inv1);
+        // fl32(lut x) as an fma with +0 (for fp16 x, one mixed-precision fma)
+        qa[i] = quant_bits(__builtin_fmaf(Pair<XT>::lo(xr[r]), lut, 0.0f), inv0);
+        qb[i] = quant_bits(__builtin_fmaf(Pair<XT>::hi(xr[r]), lut, 0.0f), inv1);
       }
       w0[r4] = pack_lo4(qa[0], qa[1], qa[2], qa[3]);
       w1[r4] = pack_lo4(qb[0], qb[1], qb[2], qb[3]);
