@@ -564,9 +564,6 @@ class SSDi8Layer:
             self.Cq = torch.empty(C.shape, dtype=torch.int8, device=x.device)
         quantize_act(B, "group", self.alpha_B, out=self.Bq, stream=stream)
         quantize_act(C, "group", self.alpha_C, out=self.Cq, stream=stream)
-        need = workspace_size(dims(Bt, L, H, G))
-        if self.workspace is None or self.workspace.numel() < need:
-            self.workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x.device)
         return ssd_chunk_scan(x, dt, self.A, self.Bq, self.Cq, self.alpha_B, self.alpha_C,
                               self.alpha_Xs, self.alpha_S, self.alpha_CB, D=self.D,
                               corr=self.corr, dt_softplus=self.dt_softplus,
