@@ -252,13 +252,8 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
       for (int i = 0; i < 4; ++i) {
         const int r = 4 * r4 + i;
         const float lut = sm.lut[jb * 32 + r];
-        // fl32(lut x) as an fma with +0: one mixed-precision fma reads the fp16 half directly
-        qa[i] = quant_bits(
-            __builtin_fmaf((float)__builtin_bit_cast(_Float16, Pair<XT>::lo(xr[r])), lut, 0.0f),
-            inv0);
-        qb[i] = quant_bits(
-            __builtin_fmaf((float)__builtin_bit_cast(_Float16, Pair<XT>::hi(xr[r])), lut, 0.0f),
-            inv1);
+        qa[i] = quant_bits(lut * (float)__builtin_bit_cast(_Float16, Pair<XT>::lo(xr[r])), inv0);
+        qb[i] = quant_bits(lut * (float)__builtin_bit_cast(_Float16, Pair<XT>::hi(xr[r])), inv1);
       }
       w0[r4] = pack_lo4(qa[0], qa[1], qa[2], qa[3]);
       w1[r4] = pack_lo4(qb[0], qb[1], qb[2], qb[3]);
