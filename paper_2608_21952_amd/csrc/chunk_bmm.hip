@@ -235,7 +235,7 @@ __global__ __launch_bounds__(kThreads) void chunk_bmm_kernel(
       const bool keep = i <= jt * 32 + jj;
       v[r] = keep ? acc[r] : 0;
       q[r] = keep ? requant_i8(v[r], s_m[jt * 32 + jj]) : 0;
-      stage[frag::cb_inblock(jj, lr)] = (int8_t)q[r];
+      stage[frag::cb_inblock(jj, lr)] = (int8_t)(q[r] ^ 0x80);   // stored as q + 128
     }
     if (cbq_tap || cb32_tap) {   // row-major debug copies
 #pragma unroll

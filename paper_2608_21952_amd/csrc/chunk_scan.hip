@@ -484,8 +484,8 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
           const int i0 = it * 32 + ks * 16 + 8 * half;
-          const uint32_t ub0 = (ks ? cur.z : cur.x) ^ 0x80808080u;
-          const uint32_t ub1 = (ks ? cur.w : cur.y) ^ 0x80808080u;
+          const uint32_t ub0 = (ks ? cur.z : cur.x);
+          const uint32_t ub1 = (ks ? cur.w : cur.y);
           float wv[8];
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
@@ -524,29 +524,28 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
           a[ks] = __builtin_bit_cast(v4i, buf_load16(cqrs, lane16, crow + 1024 * ks));
         __builtin_amdgcn_sched_barrier(0);
       }
-      // diagonal block it = jt, masked to i <= j
+      // diagonal block it = jt: its entries i > j hold the code of zero, whose weight
+      // fma(128, d, -128 d) is exactly +0, so no mask is needed
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
         const int i0 = jt * 32 + ks * 16 + 8 * half;
-        const uint32_t ub0 = (ks ? cur.z : cur.x) ^ 0x80808080u;
-        const uint32_t ub1 = (ks ? cur.w : cur.y) ^ 0x80808080u;
+        const uint32_t ub0 = (ks ? cur.z : cur.x);
+        const uint32_t ub1 = (ks ? cur.w : cur.y);
         float wv[8];
         if (diag_fast) {
           // small span: exp(cs_j - cs_i) = exp(cs_j - r_{J-1}) exp(r_{J-1} - cs_i)
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
             const float2 dd = s_dg[i0 + e];
-            const float v = __builtin_fmaf(qbyte(ub0, ub1, e), dd.x, dd.y) * ej;
-            wv[e] = (i0 + e <= jrow) ? v : 0.0f;
+            wv[e] = __builtin_fmaf(qbyte(ub0, ub1, e), dd.x, dd.y) * ej;
           }
         } else {
-          // exp per element; the clamp keeps the masked (i > j) entries finite
+          // exp per element; the clamp keeps the (zero-weight) entries i > j finite
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
             const float2 dd = s_dg[i0 + e];
             const float ex = __expf(__builtin_fminf(csrj - s_csr[i0 + e], 0.0f));
-            const float v = __builtin_fmaf(qbyte(ub0, ub1, e), dd.x, dd.y) * ex;
-            wv[e] = (i0 + e <= jrow) ? v : 0.0f;
+            wv[e] = __builtin_fmaf(qbyte(ub0, ub1, e), dd.x, dd.y) * ex;
           }
         }
         mfma_block(wv, i0);

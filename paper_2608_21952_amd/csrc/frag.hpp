@@ -16,7 +16,9 @@
 //   CB order:     the 36 causal 32x32 blocks (J, I <= J) of a 256x256 chunk; lane l of block
 //                 (J, I) holds row j = 32 J + l % 32 and the bytes i = 32 I + 16 ks + 8 (l / 32)
 //                 + e (ks = 0, 1; e < 8) in the order [ks][e]: the two K-slices of the fp16
-//                 32x32x16 ChunkScan2 B operand.
+//                 32x32x16 ChunkScan2 B operand.  The int8 codes are stored offset by 128
+//                 (unsigned byte q + 128; entries i > j hold the code of zero, byte 128),
+//                 the form in which ChunkScan2 converts them to fp16.
 #pragma once
 
 #include <hip/hip_runtime.h>
