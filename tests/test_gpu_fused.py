@@ -95,7 +95,7 @@ def test_single_pass_matches_separate_kernels_and_oracle(torch, ssdi8, cfg):
     assert np.array_equal(h["final_state_q"], ref["final_q"])
 
 
-@pytest.mark.parametrize("shift_round,shift", [(False, 7), (True, 6)])
+@pytest.mark.parametrize("shift_round,shift", [(False, 7), (True, 6), (True, 8), (False, 11)])
 def test_single_pass_variants(torch, ssdi8, shift_round, shift):
     """Initial state, floor or rounded shift of another width, per-token C steps, raw dt, no skip,
     no correction."""
