@@ -86,10 +86,72 @@ __device__ __forceinline__ uint32_t pack_lo4(uint32_t w0, uint32_t w1, uint32_t 
   return lo | (hi << 16);
 }
 
-// softplus in fp64 with the usual threshold, rounded once to fp32.
+// softplus in fp64 with the usual threshold (log1p(exp(v)) for v <= 20, v above), rounded once
+// to fp32.  On [-40, 20] a short fp64 evaluation (relative error below 2^-50) is rounded where it
+// lies at least 2^-44 (relative) from an fp32 rounding boundary, so it rounds as the exact value
+// does; elsewhere, and outside [-40, 20], the library's exp and log1p decide (Ziv's strategy).
+// The short form: softplus(d) = max(d, 0) + log1p(z), z = exp(-|d|) in (0, 1], with exp by
+// Cody-Waite reduction to |r| <= ln2 / 2 and the degree-12 Taylor polynomial, and
+// log1p(z) = log(u) + (z - (u - 1)) / u for u = fl(1 + z) (the second term restores the rounding
+// of u), log(u) = e ln2 + 2 atanh(s), s = (m - 1) / (m + 1), m = u 2^-e in (0.707, 1.414], and
+// atanh's odd series through s^19 (|s| <= 0.172).
 __device__ __forceinline__ float softplus_f32(float v) {
-  double d = (double)v;
-  return (float)(d > 20.0 ? d : log1p(exp(d)));
+  const double d = (double)v;
+  if (d > 20.0) return v;
+  bool ok = d >= -40.0;
+  float out = 0.0f;
+  if (ok) {
+    constexpr double kLn2Hi = 6.93147180369123816490e-01;   // 32 significant bits
+    constexpr double kLn2Lo = 1.90821492927058770002e-10;
+    constexpr double kLog2e = 1.4426950408889634;
+    const double x = -__builtin_fabs(d);
+    const double k = __builtin_rint(x * kLog2e);
+    double r = __builtin_fma(-k, kLn2Hi, x);
+    r = __builtin_fma(-k, kLn2Lo, r);
+    double p = 1.0 / 479001600.0;                            // 1/12!
+    p = __builtin_fma(p, r, 1.0 / 39916800.0);
+    p = __builtin_fma(p, r, 1.0 / 3628800.0);
+    p = __builtin_fma(p, r, 1.0 / 362880.0);
+    p = __builtin_fma(p, r, 1.0 / 40320.0);
+    p = __builtin_fma(p, r, 1.0 / 5040.0);
+    p = __builtin_fma(p, r, 1.0 / 720.0);
+    p = __builtin_fma(p, r, 1.0 / 120.0);
+    p = __builtin_fma(p, r, 1.0 / 24.0);
+    p = __builtin_fma(p, r, 1.0 / 6.0);
+    p = __builtin_fma(p, r, 0.5);
+    p = __builtin_fma(p, r, 1.0);
+    p = __builtin_fma(p, r, 1.0);
+    const double z = __builtin_ldexp(p, (int)k);
+    const double u = 1.0 + z;
+    const double c = z - (u - 1.0);
+    const bool big = u > 1.4142135623730951;
+    const double m = big ? u * 0.5 : u;
+    const double f = m - 1.0;
+    const double den = 2.0 + f;
+    double q = __builtin_amdgcn_rcp(den);
+    q = __builtin_fma(q, __builtin_fma(-den, q, 1.0), q);
+    const double s0 = f * q;
+    const double s = __builtin_fma(__builtin_fma(-den, s0, f), q, s0);
+    const double t = s * s;
+    double P = 2.0 / 19.0;
+    P = __builtin_fma(P, t, 2.0 / 17.0);
+    P = __builtin_fma(P, t, 2.0 / 15.0);
+    P = __builtin_fma(P, t, 2.0 / 13.0);
+    P = __builtin_fma(P, t, 2.0 / 11.0);
+    P = __builtin_fma(P, t, 2.0 / 9.0);
+    P = __builtin_fma(P, t, 2.0 / 7.0);
+    P = __builtin_fma(P, t, 2.0 / 5.0);
+    P = __builtin_fma(P, t, 2.0 / 3.0);
+    const double corr = __builtin_fma(c, __builtin_amdgcn_rcp(u), big ? kLn2Lo : 0.0);
+    const double lo = __builtin_fma(s, t * P, corr);
+    const double l1p = (big ? kLn2Hi : 0.0) + (2.0 * s + lo);
+    const double y = d > 0.0 ? d + l1p : l1p;
+    const float y0 = (float)(y * (1.0 - 0x1p-44)), y1 = (float)(y * (1.0 + 0x1p-44));
+    ok = y0 == y1;
+    out = y0;
+  }
+  if (!ok) out = (float)log1p(exp(d));
+  return out;
 }
 
 // Map a linear block id to a work index so that consecutive work items land on the same XCD.
