@@ -167,6 +167,38 @@ def test_layer_per_token_C(torch, ssdi8):
             check_slab(g, inp, sc, b, h, 256, c_scale=g["C_scale"])
 
 
+def test_layer_wide_dt_range(torch, ssdi8):
+    """Raw dt over [-45, 25] on one token in eight (both sides of the [-40, 20] domain of the
+    kernels' short fp64 softplus and of the threshold at 20, R17), with the domain edges
+    themselves at fixed tokens: the stage outputs of the separate kernels and the single pass's
+    final state match the oracle bit for bit."""
+    cfg = _small("wide-dt")
+    say(f"layer {cfg.name}")
+    inp = synth.draw(cfg, 1)
+    rng = np.random.default_rng(5)
+    dt = inp["dt_raw"].copy()
+    wide = rng.random(dt.shape) < 0.125
+    dt[wide] = rng.uniform(-45.0, 25.0, int(wide.sum())).astype(np.float32)
+    f32 = np.float32
+    edges = np.array([-40.0, np.nextafter(f32(-40.0), f32(-50.0)), 20.0,
+                      np.nextafter(f32(20.0), f32(30.0)), 0.0, -0.0, -45.0, 25.0], np.float32)
+    dt[0, 3:3 + edges.size, 1] = edges
+    dt[1, 300:300 + edges.size, 2] = edges
+    inp = dict(inp, dt_raw=dt)
+    sc = calibration(cfg)
+    # fp32 output: with dt up to 25 a few outputs exceed the fp16 range
+    g = run_layer(torch, ssdi8, inp, sc, taps=ALL_TAPS, y_dtype=torch.float32)
+    for b in range(cfg.batch):
+        for h in range(cfg.nheads):
+            check_slab(g, inp, sc, b, h, cfg.chunk, out_dtype=np.float32)
+    one = run_layer(torch, ssdi8, inp, sc, path="single", y_dtype=torch.float32)
+    ref = oq.ssdi8_forward(inp["x"], inp["dt_raw"], inp["A"], inp["B"], inp["C"], inp["D"],
+                           sc["corr"], sc, chunk=cfg.chunk, want=("y64", "final_q"))
+    assert np.isfinite(ref["y64"]).all()
+    assert np.array_equal(one["final_state_q"], ref["final_q"])
+    assert_close(one["y"], ref["y64"], "y (single pass, wide dt)")
+
+
 @pytest.mark.parametrize("shift_round", [True, False])
 def test_layer_floor_or_round_shift_and_init_state(torch, ssdi8, shift_round):
     cfg = _small("init", seqlen=768)
