@@ -172,6 +172,10 @@ typedef struct {
      results are identical to quantizing first and passing Bq / Cq; the row-major int8 B, C
      are then never written. */
   const void* B; const void* C; int bc_dtype;
+  /* Optional intermediate output like the taps above (NULL = not produced; requesting it selects
+     the separate kernels): [B,L,H] fp32 dt as the kernels use it, i.e. after the softplus when
+     dt_softplus != 0 (Alg. 2 module 1: fl32 of the fp64 softplus, threshold 20). */
+  float* dt_post;
 } ssdi8_scan_args;
 
 /* Workspace bytes needed by ssdi8_ssd_chunk_scan for these sizes (0 on invalid sizes). */

@@ -122,8 +122,8 @@ ssdi8_status check_dims(const ssdi8_dims* d) {
 
 // Whether ssdi8_ssd_chunk_scan runs ChunkState, StatePassing and ChunkScan as the single pass.
 bool single_pass(const ssdi8_dims* d, const ssdi8_scan_args* a) {
-  const bool eligible = a->x_dtype == SSDI8_F16 && !a->xs_q && !a->state_i32 && !a->state_q &&
-                        !a->decay_q && !a->state_in_q && !a->scan1_i32;
+  const bool eligible = a->x_dtype == SSDI8_F16 && !a->xs_q && !a->dt_post && !a->state_i32 &&
+                        !a->state_q && !a->decay_q && !a->state_in_q && !a->scan1_i32;
   if (!eligible) return false;
   if (a->path != 0) return a->path == 2;
   // automatic: the single pass hides its chain of nc hand-offs behind enough concurrent
@@ -233,7 +233,8 @@ ssdi8_status ssdi8_ssd_chunk_scan(const ssdi8_dims* d, const ssdi8_scan_args* a,
   if (a->final_state && !a->state_scale) return SSDI8_ERR_NULL;
   const void* al[] = {a->x, a->y, a->Bq, a->Cq, a->B, a->C, a->init_state_q, a->final_state_q,
                       a->final_state, a->xs_q, a->state_i32, a->state_q, a->decay_q,
-                      a->state_in_q, a->cb_i32, a->cb_q, a->scan1_i32, a->workspace};
+                      a->state_in_q, a->cb_i32, a->cb_q, a->scan1_i32, a->dt_post,
+                      a->workspace};
   for (const void* p : al)
     if (!aligned16_or_null(p)) return SSDI8_ERR_ALIGN;
   const Plan plan = plan_workspace(d);
@@ -310,7 +311,8 @@ ssdi8_status ssdi8_ssd_chunk_scan(const ssdi8_dims* d, const ssdi8_scan_args* a,
   }
   e = ssdi8::launch_chunk_state(ld, a->x, a->x_dtype, a->dt, a->dt_softplus, a->A, bqT,
                                 a->B_scale, a->xs_scale, a->xs_per_head, a->state_scale,
-                                a->decay_shift, sq, qd, a->xs_q, a->state_q, a->state_i32, st);
+                                a->decay_shift, sq, qd, a->xs_q, a->state_q, a->state_i32,
+                                a->dt_post, st);
   if (e != hipSuccess || !mark(2)) return SSDI8_ERR_HIP;
   e = ssdi8::launch_state_pass(d->batch, ld.nchunks, d->nheads, elems, d->headdim, sq, qd,
                                a->decay_shift, a->shift_round, a->init_state_q, pin,

@@ -58,7 +58,7 @@ __global__ __launch_bounds__(256, sizeof(XT) == 2 ? 6 : 4) void chunk_state_kern
     const float* __restrict__ xs_scale, int xs_per_head, const float* __restrict__ state_scale,
     int dt_softplus, int shift, int8_t* __restrict__ sq, int16_t* __restrict__ qd,
     int8_t* __restrict__ xq_tap, int8_t* __restrict__ sq_tap, int32_t* __restrict__ s32_tap,
-    int L, int H, int G, int nc) {
+    float* __restrict__ dt_tap, int L, int H, int G, int nc) {
   __shared__ __attribute__((aligned(16))) int8_t s_xq[kP * kXS];
   __shared__ float s_lut[kQ];
   __shared__ float s_inv[kP];
@@ -89,6 +89,7 @@ __global__ __launch_bounds__(256, sizeof(XT) == 2 ? 6 : 4) void chunk_state_kern
   // ---- ChunkCumsum: token t
   float dtv = dt[(tok0 + t) * H + h];
   if (dt_softplus) dtv = softplus_f32(dtv);
+  if (dt_tap) dt_tap[(tok0 + t) * H + h] = dtv;
   const float dA = dtv * A[h];
   const double cs = block_scan_f64_256((double)dA, s_scan);
   if (t == kQ - 1) s_last = cs;
@@ -201,18 +202,19 @@ hipError_t launch_chunk_state(const LayerDims& d, const void* x, int x_dtype, co
                               int dt_softplus, const float* A, const int8_t* bqT,
                               const float* B_scale, const float* xs_scale, int xs_per_head,
                               const float* state_scale, int shift, int8_t* sq, int16_t* qd,
-                              int8_t* xq_tap, int8_t* sq_tap, int32_t* s32_tap, hipStream_t st) {
+                              int8_t* xq_tap, int8_t* sq_tap, int32_t* s32_tap, float* dt_tap,
+                              hipStream_t st) {
   const int64_t nwork = (int64_t)d.batch * d.nchunks * d.nheads;
   if (nwork == 0) return hipSuccess;
   if (x_dtype == 1) {
     hipLaunchKernelGGL(chunk_state_kernel<_Float16>, dim3((unsigned)nwork), dim3(256), 0, st,
                        static_cast<const _Float16*>(x), dt, A, bqT, B_scale, xs_scale,
                        xs_per_head, state_scale, dt_softplus, shift, sq, qd, xq_tap, sq_tap,
-                       s32_tap, d.seqlen, d.nheads, d.ngroups, d.nchunks);
+                       s32_tap, dt_tap, d.seqlen, d.nheads, d.ngroups, d.nchunks);
   } else {
     hipLaunchKernelGGL(chunk_state_kernel<float>, dim3((unsigned)nwork), dim3(256), 0, st,
                        static_cast<const float*>(x), dt, A, bqT, B_scale, xs_scale, xs_per_head,
-                       state_scale, dt_softplus, shift, sq, qd, xq_tap, sq_tap, s32_tap,
+                       state_scale, dt_softplus, shift, sq, qd, xq_tap, sq_tap, s32_tap, dt_tap,
                        d.seqlen, d.nheads, d.ngroups, d.nchunks);
   }
   return hipGetLastError();

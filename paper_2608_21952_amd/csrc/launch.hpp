@@ -37,7 +37,8 @@ hipError_t launch_chunk_state(const LayerDims& d, const void* x, int x_dtype, co
                               int dt_softplus, const float* A, const int8_t* bqT,
                               const float* B_scale, const float* xs_scale, int xs_per_head,
                               const float* state_scale, int shift, int8_t* sq, int16_t* qd,
-                              int8_t* xq_tap, int8_t* sq_tap, int32_t* s32_tap, hipStream_t st);
+                              int8_t* xq_tap, int8_t* sq_tap, int32_t* s32_tap, float* dt_tap,
+                              hipStream_t st);
 
 // INT8 StatePassing (Eq. 9) over [b, c, h, elems] slabs with elems = P*N (any P*N % 4 == 0).
 // frag_k = 0: S_q and P_in row-major; frag_k = N: both in kslice order with K = N (P, N

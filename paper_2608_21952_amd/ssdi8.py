@@ -48,7 +48,7 @@ class ScanArgs(ctypes.Structure):
         ("cb_i32", _P), ("cb_q", _P), ("scan1_i32", _P),
         ("workspace", _P), ("workspace_bytes", ctypes.c_size_t),
         ("stage_events", _P), ("path", _I),
-        ("B", _P), ("C", _P), ("bc_dtype", _I),
+        ("B", _P), ("C", _P), ("bc_dtype", _I), ("dt_post", _P),
     ]
 
 
@@ -239,6 +239,7 @@ def workspace_size(d: Dims) -> int:
 
 TAPS = {  # name -> (dtype, shape builder(B, L, H, P, G, N, Q, c))
     "xs_q": (torch.int8, lambda B, L, H, P, G, N, Q, c: (B, L, H, P)),
+    "dt_post": (torch.float32, lambda B, L, H, P, G, N, Q, c: (B, L, H)),
     "state_i32": (torch.int32, lambda B, L, H, P, G, N, Q, c: (B, c, H, P, N)),
     "state_q": (torch.int8, lambda B, L, H, P, G, N, Q, c: (B, c, H, P, N)),
     "decay_q": (torch.int16, lambda B, L, H, P, G, N, Q, c: (B, H, c)),

@@ -199,6 +199,55 @@ def test_layer_wide_dt_range(torch, ssdi8):
     assert_close(one["y"], ref["y64"], "y (single pass, wide dt)")
 
 
+def _softplus_near_boundary(n_draw=1 << 24, rel=2.0 ** -44, seed=9):
+    """Raw fp32 dt values whose fp64 softplus lies within `rel` (relative) of an fp32 rounding
+    boundary: there the kernels' short softplus defers to the library's exp and log1p."""
+    rng = np.random.default_rng(seed)
+    x = rng.uniform(-30.0, 19.0, n_draw).astype(np.float32)
+    v = oq.softplus64(x)
+    m = v.astype(np.float32)
+    dist = np.full(v.shape, np.inf)
+    for nb in (np.nextafter(m, np.float32(np.inf)), np.nextafter(m, np.float32(-np.inf))):
+        dist = np.minimum(dist, np.abs(v - (m.astype(np.float64) + nb.astype(np.float64)) / 2))
+    return x[dist < rel * v]
+
+
+def test_softplus_tap_bitexact(torch, ssdi8):
+    """The dt the kernels use (tap dt_post) is fl32 of the fp64 softplus (R17) on every token:
+    raw dt over [-45, 25], the edges of the short form's domain [-40, 20], and inputs next to an
+    fp32 rounding boundary, where the short form defers to the library.  Only values that are
+    ambiguous within a few fp64 ulps (the oracle's fragile rule) may differ."""
+    cfg = _small("softplus-tap", batch=1, seqlen=4096, nheads=4)
+    inp = synth.draw(cfg, 1)
+    near = _softplus_near_boundary()
+    say(f"softplus tap: {near.size} near-boundary inputs")
+    assert near.size >= 4
+    f32 = np.float32
+    edges = np.array([-40.0, np.nextafter(f32(-40.0), f32(-50.0)), 20.0,
+                      np.nextafter(f32(20.0), f32(30.0)), np.nextafter(f32(20.0), f32(0.0)),
+                      0.0, -0.0, -45.0, 25.0, -1e-30, 1e-30], np.float32)
+    dt = inp["dt_raw"].copy()
+    flat = dt.reshape(-1)
+    rng = np.random.default_rng(6)
+    wide = rng.random(flat.shape) < 0.25
+    flat[wide] = rng.uniform(-45.0, 25.0, int(wide.sum())).astype(np.float32)
+    flat[:near.size] = near
+    flat[near.size:near.size + edges.size] = edges
+    inp = dict(inp, dt_raw=dt)
+    sc = calibration(cfg)
+    g = run_layer(torch, ssdi8, inp, sc, taps=("dt_post",), y_dtype=torch.float32)
+    ref = oq.dt_post(dt, True)
+    fragile = oq._ambiguous_fp32(oq.softplus64(dt)) & (dt <= 20.0)
+    diff = g["dt_post"] != ref
+    assert not np.any(diff & ~fragile), f"dt differs at {np.argwhere(diff & ~fragile)[:5]}"
+    say(f"  {int(fragile.sum())} fragile, {int(diff.sum())} differ")
+    raw = g["dt_post"].copy()
+    g0 = run_layer(torch, ssdi8, inp, sc, taps=("dt_post",), dt_softplus=False,
+                   y_dtype=torch.float32)
+    assert np.array_equal(g0["dt_post"].view(np.uint32), dt.view(np.uint32))
+    assert np.all(np.isfinite(raw))
+
+
 @pytest.mark.parametrize("shift_round", [True, False])
 def test_layer_floor_or_round_shift_and_init_state(torch, ssdi8, shift_round):
     cfg = _small("init", seqlen=768)
