@@ -62,11 +62,19 @@ def algorithmic_bytes(cfg, quant_in_bmm=False):
         "chunk_state": T * H * P * sx + T * H * 4 + T * G * N + states + B * H * c * 2,
         "state_pass": 2 * states + B * H * c * 2 + B * H * P * N * 5,
         "chunk_scan": 2 * T * H * P * sx + T * H * 4 + T * G * N + states + cb_causal,
-        # x in, y out, dt, B_q^T and C_q (per group), CB_q, the entering states handed from
-        # chunk to chunk (written once, read once) and the final state (int8 + fp32)
+        # x in, y out, dt, B_q^T and C_q (per group), CB_q and the final state (int8 + fp32);
+        # the states handed from chunk to chunk are overhead (single_pass_overhead)
         "single_pass": (2 * T * H * P * sx + T * H * 4 + 2 * T * G * N + cb_causal
-                        + 2 * B * (c - 1) * H * P * N + B * H * P * N * 5),
+                        + B * H * P * N * 5),
     }
+
+
+def single_pass_overhead(cfg):
+    """Bytes the single pass moves beyond the minimum of its inputs and outputs: the int8 state
+    entering each chunk after the first, written by the chunk before it and read once."""
+    B, L, H, P, N, Q = cfg.batch, cfg.seqlen, cfg.nheads, cfg.headdim, cfg.dstate, cfg.chunk
+    c = L // Q
+    return {"hand_off_states": 2 * B * max(c - 1, 0) * H * P * N}
 
 
 def algorithmic_ops(cfg):
@@ -86,7 +94,8 @@ def algorithmic_ops(cfg):
 
 
 def layer_min_bytes(cfg):
-    """Layer-level minimum: x, dt, B, C in; y and the final state out."""
+    """Layer-level minimum, per token: x in and y out (H P elements each), dt (4 H bytes), B and C
+    at the input width (2 G N elements); plus the final state (int8 and fp32, 5 B H P N)."""
     B, L, H, P, G, N = cfg.batch, cfg.seqlen, cfg.nheads, cfg.headdim, cfg.ngroups, cfg.dstate
     sx = 2 if cfg.dtype == "fp16" else 4
     T = B * L
@@ -313,7 +322,9 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="mamba2-130m")
+    ap.add_argument("--workload", default="long-64k",
+                    help="one of the synthetic layers; the default is the largest one-GPU "
+                         "workload (65536 tokens x 80 heads)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget-s", type=float, default=15.0)
     ap.add_argument("--eager", action="store_true",
@@ -472,7 +483,10 @@ def main():
             stages[n]["fp16_tflops"] = round(f16 / sec / 1e12, 1)
             stages[n]["fp16_mfma_frac"] = round(f16 / sec / 1e12 / FP16_PEAK_TFLOPS, 4)
     dom = "single_pass" if single else "chunk_scan"
-    ach = abytes[dom] / (per[dom] * 1e-3) / 1e9
+    # the single pass runs every step of the layer after ChunkBMM: its roofline takes the layer's
+    # minimum bytes (B and C at the input width); the separate path's ChunkScan its own minimum
+    rbytes = layer_min_bytes(cfg) if single else abytes[dom]
+    ach = rbytes / (per[dom] * 1e-3) / 1e9
     tokens = cfg.batch * cfg.seqlen
     value = tokens / (ms_step * 1e-3)
     traffic = measured_traffic(dom, cfg.name)
@@ -487,7 +501,12 @@ def main():
                    "ngroups": cfg.ngroups, "chunk": cfg.chunk, "io_dtype": cfg.dtype},
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(ach, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4),
-                     "traffic": traffic, "algorithmic_bytes": abytes[dom],
+                     "traffic": traffic, "algorithmic_bytes": rbytes,
+                     "basis": ("layer minimum: x in, y out, dt, B and C at the input width, "
+                               "final state" if single else
+                               "ChunkScan minimum: x in, y out, dt, C_q, CB_q, P_in"),
+                     "kernel_min_bytes": abytes[dom],
+                     "overhead_bytes": single_pass_overhead(cfg) if single else {},
                      "avg_us": round(per[dom] * 1e3, 2)},
         "timing": ("K replays of one captured HIP graph; per-kernel times from K eager steps "
                    "bracketed by HIP events" if graph is not None else "eager launches"),
@@ -534,8 +553,8 @@ def main():
                 % Kc,
         "ms_per_step": round(cms, 4), "tokens_per_s": tokens / (cms * 1e-3),
         "dominant_kernel_us": round(cdom * 1e3, 2),
-        "dominant_kernel_GBps": round(abytes[dom] / (cdom * 1e-3) / 1e9, 1),
-        "dominant_kernel_hbm_frac": round(abytes[dom] / (cdom * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+        "dominant_kernel_GBps": round(rbytes / (cdom * 1e-3) / 1e9, 1),
+        "dominant_kernel_hbm_frac": round(rbytes / (cdom * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
     peaks = measured_peaks(torch, ssdi8)
     result["measured_peaks"] = peaks
     result["roofline"]["frac_of_measured_copy"] = round(ach / peaks["hbm_copy_GBps"], 4)

@@ -156,14 +156,15 @@ typedef struct {
      ChunkScan and after ChunkScan (the module breakdown of the paper's latency figures).
      Leave NULL when the call is captured into a HIP graph. */
   void* const* stage_events;
-  /* Kernel path.  With fp16 x and none of the taps xs_q, state_i32, state_q, decay_q, state_in_q,
-     scan1_i32 requested, ChunkState, StatePassing and ChunkScan can run as one single-pass
-     kernel in which each chunk waits for the previous chunk of its sequence to hand over the
-     int8 entering state (integer results identical; y differs from the separate kernels only by
-     the rounding of ChunkScan's fp32 tables).  0: automatic (the single pass where it is the
-     faster one, which takes enough concurrent sequences to hide the serial chain of hand-offs:
-     batch * nheads >= 192 with at least 4 chunks, >= 128 with at least 16, or >= 80 with at
-     least 32); 1: always the separate kernels; 2: the single pass whenever eligible.
+  /* Kernel path.  With fp16 x and none of the taps xs_q, state_i32, state_q, decay_q, scan1_i32,
+     dt_post requested, ChunkState, StatePassing and ChunkScan can run as one single-pass kernel
+     in which each chunk obtains the int8 state entering it from the chunks before it in its
+     sequence through the workspace (a flag per chunk; Eq. 9 applied in chunk order, so every
+     integer result and y are bit-identical to the separate kernels).  The state_in_q tap is
+     served by either path.  0: automatic (the single pass where it is the faster one, which
+     takes enough concurrent sequences to hide the serial hand-offs: batch * nheads >= 192 with
+     at least 4 chunks, >= 128 with at least 16, or >= 80 with at least 32); 1: always the
+     separate kernels; 2: the single pass whenever eligible.
      With the single pass, events 1-3 of stage_events are recorded back to back before it. */
   int path;
   /* Alternative to Bq / Cq (both NULL then): the unquantized B, C [B,L,G,N] of bc_dtype
@@ -176,6 +177,14 @@ typedef struct {
      the separate kernels): [B,L,H] fp32 dt as the kernels use it, i.e. after the softplus when
      dt_softplus != 0 (Alg. 2 module 1: fl32 of the fp64 softplus, threshold 20). */
   float* dt_post;
+  /* Optional device int (4-byte aligned), or NULL.  A single-pass workgroup waits for the
+     states of earlier chunks of its sequence with a bounded poll (2^16 polls, tens of ms); a
+     wait that runs out is counted here and the kernel still finishes, but y and the final
+     states of that layer are then unspecified.  The count is set to 0 by the call's first
+     kernel and is 0 after the separate kernels, which never wait.  Read it after the stream
+     has reached the end of the call; non-zero means the results must not be used (the GPU was
+     preempted or shared for longer than the bound). */
+  int* hand_off_timeouts;
 } ssdi8_scan_args;
 
 /* Workspace bytes needed by ssdi8_ssd_chunk_scan for these sizes (0 on invalid sizes). */
@@ -185,8 +194,12 @@ size_t ssdi8_ssd_workspace_size(const ssdi8_dims* d);
  * ssdi8_ssd_chunk_scan — one SSD layer: ChunkCumsum, ChunkState, StatePassing, ChunkBMM,
  * ChunkScan1 + ChunkScan2 and the output epilogue
  *     y = y_off + y_diag + D[h] x + corr[h, p]
- * (Alg. 2 modules 1-6, Eq. 7-9, Eq. 10 correction applied at the SSD output).  B and C must
- * already be quantized (ssdi8_quantize_act).  Intermediates go through `workspace`.
+ * (Alg. 2 modules 1-6, Eq. 7-9, Eq. 10 correction applied at the SSD output).  B and C arrive
+ * either quantized (Bq, Cq from ssdi8_quantize_act with per-group steps) or unquantized (B, C
+ * of bc_dtype with Bq = Cq = NULL); in the second form ChunkBMM quantizes each row with the
+ * static steps B_scale, C_scale as it loads it (Sec. 4.2: B and C quantized once, before any
+ * reuse), bit-identically to calling ssdi8_quantize_act first, and the row-major int8 copies
+ * are never written.  Intermediates go through `workspace`.
  */
 ssdi8_status ssdi8_ssd_chunk_scan(const ssdi8_dims* d, const ssdi8_scan_args* a, void* stream);
 

@@ -122,8 +122,10 @@ ssdi8_status check_dims(const ssdi8_dims* d) {
 
 // Whether ssdi8_ssd_chunk_scan runs ChunkState, StatePassing and ChunkScan as the single pass.
 bool single_pass(const ssdi8_dims* d, const ssdi8_scan_args* a) {
+  // the entering states (state_in_q) are in the workspace either way; the other taps are
+  // intermediates only the separate kernels hold
   const bool eligible = a->x_dtype == SSDI8_F16 && !a->xs_q && !a->dt_post && !a->state_i32 &&
-                        !a->state_q && !a->decay_q && !a->state_in_q && !a->scan1_i32;
+                        !a->state_q && !a->decay_q && !a->scan1_i32;
   if (!eligible) return false;
   if (a->path != 0) return a->path == 2;
   // automatic: the single pass hides its chain of nc hand-offs behind enough concurrent
@@ -231,6 +233,7 @@ ssdi8_status ssdi8_ssd_chunk_scan(const ssdi8_dims* d, const ssdi8_scan_args* a,
                !a->xs_scale || !a->state_scale || !a->cb_scale || !a->y))
     return SSDI8_ERR_NULL;
   if (a->final_state && !a->state_scale) return SSDI8_ERR_NULL;
+  if ((uintptr_t)a->hand_off_timeouts & 3u) return SSDI8_ERR_ALIGN;
   const void* al[] = {a->x, a->y, a->Bq, a->Cq, a->B, a->C, a->init_state_q, a->final_state_q,
                       a->final_state, a->xs_q, a->state_i32, a->state_q, a->decay_q,
                       a->state_in_q, a->cb_i32, a->cb_q, a->scan1_i32, a->dt_post,
@@ -284,7 +287,7 @@ ssdi8_status ssdi8_ssd_chunk_scan(const ssdi8_dims* d, const ssdi8_scan_args* a,
                                          a->C_scale, a->c_per_token,
                                          a->B_scale, a->cb_scale, cbq, a->cb_q, a->cb_i32, bqT,
                                          cq, fused ? 1 : 0, sync, fused ? (int)plan.nsync : 0,
-                                         st);
+                                         a->hand_off_timeouts, st);
   if (e != hipSuccess || !mark(1)) return SSDI8_ERR_HIP;
   if (fused) {
     if (!mark(2) || !mark(3)) return SSDI8_ERR_HIP;
@@ -299,6 +302,7 @@ ssdi8_status ssdi8_ssd_chunk_scan(const ssdi8_dims* d, const ssdi8_scan_args* a,
     fs.final_q = a->final_state_q;
     fs.final_state = a->final_state;
     fs.sync = sync;
+    fs.timeouts = a->hand_off_timeouts;
     fs.nbh = ld.batch * ld.nheads;
     fs.nclass = ssdi8::sync_classes(fs.nbh);
     fs.spin_limit = 1 << 16;   // polls of ~1 us: a wait gives up after ~65 ms
@@ -307,6 +311,11 @@ ssdi8_status ssdi8_ssd_chunk_scan(const ssdi8_dims* d, const ssdi8_scan_args* a,
                                        cbq, a->cb_scale, a->state_scale, a->D, a->corr, a->y,
                                        a->y_dtype, fs, st);
     if (e != hipSuccess || !mark(4)) return SSDI8_ERR_HIP;
+    if (a->state_in_q) {
+      e = ssdi8::launch_pin_tap(pin, a->state_in_q, (int64_t)ld.batch * ld.nchunks * ld.nheads,
+                                st);
+      if (e != hipSuccess) return SSDI8_ERR_HIP;
+    }
     return SSDI8_OK;
   }
   e = ssdi8::launch_chunk_state(ld, a->x, a->x_dtype, a->dt, a->dt_softplus, a->A, bqT,

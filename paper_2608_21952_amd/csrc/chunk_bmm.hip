@@ -96,8 +96,8 @@ __global__ __launch_bounds__(kThreads) void chunk_bmm_kernel(
     const float* __restrict__ C_scale, int c_per_token, const float* __restrict__ B_scale,
     const float* __restrict__ cb_scale, int8_t* __restrict__ cbq_frag,
     int8_t* __restrict__ cbq_tap, int32_t* __restrict__ cb32_tap, int8_t* __restrict__ bqT_frag,
-    int8_t* __restrict__ cq_frag, int cq_perm, int* __restrict__ sync, int nsync, int L, int G,
-    int nc, int S) {
+    int8_t* __restrict__ cq_frag, int cq_perm, int* __restrict__ sync, int nsync,
+    int* __restrict__ timeouts, int L, int G, int nc, int S) {
   __shared__ __attribute__((aligned(16))) int8_t s_c[kQ * kN];
   __shared__ __attribute__((aligned(16))) int8_t s_b[kQ * kN];
   __shared__ __attribute__((aligned(16))) int8_t s_stage[kWaves * 1024];
@@ -107,6 +107,8 @@ __global__ __launch_bounds__(kThreads) void chunk_bmm_kernel(
   const int wv = __builtin_amdgcn_readfirstlane(t >> 6);
   // clears the ticket and hand-off flags of the single-pass scan that follows in the stream
   for (int i = blockIdx.x * kThreads + t; i < nsync; i += gridDim.x * kThreads) sync[i] = 0;
+  // and the caller's count of hand-off waits that ran out (0 after the separate kernels)
+  if (timeouts && blockIdx.x == 0 && t == 0) *timeouts = 0;
   const int w = xcd_remap(blockIdx.x, gridDim.x);
   const int part = w % S;
   const int g = (w / S) % G;
@@ -263,7 +265,7 @@ hipError_t launch_chunk_bmm(const LayerDims& d, const void* C, const void* B, in
                             const float* C_scale, int c_per_token, const float* B_scale,
                             const float* cb_scale, int8_t* cbq_frag, int8_t* cbq_tap,
                             int32_t* cb32_tap, int8_t* bqT_frag, int8_t* cq_frag, int cq_perm,
-                            int* sync, int nsync, hipStream_t st) {
+                            int* sync, int nsync, int* timeouts, hipStream_t st) {
   const int64_t ncg = (int64_t)d.batch * d.nchunks * d.ngroups;
   // parts per chunk-group: enough workgroups to reach every CU on small layers
   const int S = ncg <= 128 ? 4 : (ncg <= 256 ? 2 : 1);
@@ -273,7 +275,7 @@ hipError_t launch_chunk_bmm(const LayerDims& d, const void* C, const void* B, in
   hipLaunchKernelGGL(chunk_bmm_kernel<T>, dim3((unsigned)nwork), dim3(kThreads), 0, st,        \
                      static_cast<const T*>(C), static_cast<const T*>(B), C_scale, c_per_token,  \
                      B_scale, cb_scale, cbq_frag, cbq_tap, cb32_tap, bqT_frag, cq_frag,         \
-                     cq_perm, sync, nsync, d.seqlen, d.ngroups, d.nchunks, S)
+                     cq_perm, sync, nsync, timeouts, d.seqlen, d.ngroups, d.nchunks, S)
   if (src_dtype < 0) SSDI8_BMM_LAUNCH(int8_t);
   else if (src_dtype == 1) SSDI8_BMM_LAUNCH(_Float16);
   else SSDI8_BMM_LAUNCH(float);

@@ -62,16 +62,6 @@ template <> struct Pair<float> {
   }
 };
 
-// softplus to a few fp32 ulps (the output path only needs dt to fp32 accuracy): log1p(e) for
-// e = exp(v) as log(u) * e / (u - 1) with u = fl(1 + e), which cancels the rounding of u.
-__device__ __forceinline__ float softplus_fast(float v) {
-  const float e = __expf(v);
-  const float u = 1.0f + e;
-  const float d = u - 1.0f;
-  const float lp = (d == 0.0f) ? e : __logf(u) * (e / d);
-  return v > 20.0f ? v : lp;
-}
-
 template <typename XT, typename YT, bool kFused>
 __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
     const XT* __restrict__ x, const float* __restrict__ dt, const float* __restrict__ A,
@@ -182,9 +172,10 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
 #pragma unroll
     for (int r = 0; r < 32; ++r) xr[r] = Pair<XT>::load(xrs, xo, (uint32_t)(r * HP * sizeof(XT)));
   }
-  // ---- ChunkCumsum (fp64 sums; the factors derived from it only need fp32 accuracy here)
-  // the single pass quantizes X_scaled, which needs the fp64 softplus of ChunkState
-  if (dt_softplus) dtv = kFused ? softplus_f32(dtv) : softplus_fast(dtv);
+  // ---- ChunkCumsum (fp64 sums; the factors derived from it only need fp32 accuracy here).
+  //      dt is the fp64 softplus rounded once to fp32, as in ChunkState: one dt per token for
+  //      the whole layer (and X_scaled of the single pass needs exactly that value)
+  if (dt_softplus) dtv = softplus_f32(dtv);
   const float dA = dtv * A[h];
   const double cs = block_scan_f64_256((double)dA, s_scan);
   if ((t & 31) == 31) s_r[t >> 5] = cs;
@@ -328,7 +319,10 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
         }
         __builtin_amdgcn_s_sleep(2);
       }
-      if (!ok) atomicAdd(fs.sync + kSyncWait, 1);
+      if (!ok) {
+        atomicAdd(fs.sync + kSyncWait, 1);
+        if (fs.timeouts) atomicAdd(fs.timeouts, 1);
+      }
     }
     __syncthreads();
     {

@@ -40,14 +40,6 @@ template <> struct Pair<float> {
   }
 };
 
-__device__ __forceinline__ float softplus_fast(float v) {
-  const float e = __expf(v);
-  const float u = 1.0f + e;
-  const float d = u - 1.0f;
-  const float lp = (d == 0.0f) ? e : __logf(u) * (e / d);
-  return v > 20.0f ? v : lp;
-}
-
 // 8 fp32 -> 8 fp16
 __device__ __forceinline__ v8h to_h8(uint4 a, uint4 b) {
   typedef float f2_t __attribute__((ext_vector_type(2)));
@@ -109,7 +101,7 @@ __global__ __launch_bounds__(256, 3) void fp16_scan_kernel(
   }
 
   float dtv = dt[(tok0 + t) * H + h];
-  if (dt_softplus) dtv = softplus_fast(dtv);
+  if (dt_softplus) dtv = softplus_f32(dtv);   // the dt of this layer's ChunkState
   const float dA = dtv * A[h];
   const double cs = block_scan_f64_256((double)dA, sm.scan);
   if ((t & 31) == 31) s_r[t >> 5] = cs;

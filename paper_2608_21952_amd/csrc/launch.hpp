@@ -30,7 +30,7 @@ hipError_t launch_chunk_bmm(const LayerDims& d, const void* C, const void* B, in
                             const float* C_scale, int c_per_token, const float* B_scale,
                             const float* cb_scale, int8_t* cbq_frag, int8_t* cbq_tap,
                             int32_t* cb32_tap, int8_t* bqT_frag, int8_t* cq_frag, int cq_perm,
-                            int* sync, int nsync, hipStream_t st);
+                            int* sync, int nsync, int* timeouts, hipStream_t st);
 
 // ChunkCumsum + reformulated ChunkState (Eq. 7-8) and Q(Decay) (Eq. 9).
 hipError_t launch_chunk_state(const LayerDims& d, const void* x, int x_dtype, const float* dt,
@@ -39,6 +39,10 @@ hipError_t launch_chunk_state(const LayerDims& d, const void* x, int x_dtype, co
                               const float* state_scale, int shift, int8_t* sq, int16_t* qd,
                               int8_t* xq_tap, int8_t* sq_tap, int32_t* s32_tap, float* dt_tap,
                               hipStream_t st);
+
+// The entering states P_in[c] the single pass leaves in the workspace (permuted kslice order,
+// one P x N slab per (b, c, h)) as the row-major [b, c, h, p, n] tap.
+hipError_t launch_pin_tap(const int8_t* pin, int8_t* tap, int64_t nslabs, hipStream_t st);
 
 // INT8 StatePassing (Eq. 9) over [b, c, h, elems] slabs with elems = P*N (any P*N % 4 == 0).
 // frag_k = 0: S_q and P_in row-major; frag_k = N: both in kslice order with K = N (P, N
@@ -87,6 +91,7 @@ struct FusedState {
   int8_t* final_q = nullptr;
   float* final_state = nullptr;
   int* sync = nullptr;
+  int* timeouts = nullptr;   // the caller's count of waits that ran out, or NULL
   int nbh = 0;
   int nclass = 8;       // sync_classes(nbh)
   int spin_limit = 0;

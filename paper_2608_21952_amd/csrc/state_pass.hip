@@ -128,7 +128,33 @@ __global__ __launch_bounds__(256) void state_pass_kernel(
   }
 }
 
+// One 16-byte lane slice of a permuted-kslice P x N slab per thread: row p = 32 (tile / 4) +
+// lane % 32, and four runs of four consecutive n at 32 (tile % 4) + 8 g + 4 (lane / 32).
+__global__ __launch_bounds__(256) void pin_tap_kernel(const int8_t* __restrict__ pin,
+                                                      int8_t* __restrict__ tap, int64_t nslices) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= nslices) return;
+  constexpr int64_t kSlab = (int64_t)kP * kN;
+  const int64_t slab = i / (kSlab / 16);
+  const int off = (int)(i - slab * (kSlab / 16)) * 16;
+  const uint4 v = *reinterpret_cast<const uint4*>(pin + slab * kSlab + off);
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+  int row, k;
+  frag::pk_coords((size_t)off, kN, &row, &k);   // k of byte 0; byte 4 g at k + 8 g
+  int8_t* dst = tap + slab * kSlab + (int64_t)row * kN + k;
+#pragma unroll
+  for (int g = 0; g < 4; ++g) *reinterpret_cast<uint32_t*>(dst + 8 * g) = w[g];
+}
+
 }  // namespace
+
+hipError_t launch_pin_tap(const int8_t* pin, int8_t* tap, int64_t nslabs, hipStream_t st) {
+  const int64_t nslices = nslabs * ((int64_t)kP * kN / 16);
+  if (nslices == 0) return hipSuccess;
+  hipLaunchKernelGGL(pin_tap_kernel, dim3((unsigned)((nslices + 255) / 256)), dim3(256), 0, st,
+                     pin, tap, nslices);
+  return hipGetLastError();
+}
 
 hipError_t launch_state_pass(int64_t batch, int64_t nchunks, int64_t nheads, int64_t elems,
                              int64_t headdim, const int8_t* sq, const int16_t* qd, int shift,

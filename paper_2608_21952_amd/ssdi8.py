@@ -48,7 +48,7 @@ class ScanArgs(ctypes.Structure):
         ("cb_i32", _P), ("cb_q", _P), ("scan1_i32", _P),
         ("workspace", _P), ("workspace_bytes", ctypes.c_size_t),
         ("stage_events", _P), ("path", _I),
-        ("B", _P), ("C", _P), ("bc_dtype", _I), ("dt_post", _P),
+        ("B", _P), ("C", _P), ("bc_dtype", _I), ("dt_post", _P), ("hand_off_timeouts", _P),
     ]
 
 
@@ -261,7 +261,8 @@ def ssd_chunk_scan(x: torch.Tensor, dt: torch.Tensor, A: torch.Tensor,
                    taps: Iterable[str] = (), workspace: Optional[torch.Tensor] = None,
                    y: Optional[torch.Tensor] = None, stage_events=None,
                    path: str = "auto", B: Optional[torch.Tensor] = None,
-                   C: Optional[torch.Tensor] = None, stream=None) -> Dict[str, torch.Tensor]:
+                   C: Optional[torch.Tensor] = None, stream=None,
+                   hand_off_timeouts: Optional[torch.Tensor] = None) -> Dict[str, torch.Tensor]:
     """One SSDi8 SSD layer (ssdi8_ssd_chunk_scan).  Shapes: x (B,L,H,P), dt (B,L,H), A (H),
     Bq/Cq (B,L,G,N) int8 -- or Bq = Cq = None and B, C (B,L,G,N) fp16/fp32 unquantized, then
     quantized with the static B_scale, C_scale inside ChunkBMM --, B_scale (G), C_scale (G) or
@@ -270,7 +271,9 @@ def ssd_chunk_scan(x: torch.Tensor, dt: torch.Tensor, A: torch.Tensor,
     Returns y, final_state_q, final_state and the requested taps (zero-initialised tensors,
     so entries a stage does not write, such as C.B^T above the diagonal, read as 0).
     path: "auto", "separate" (ChunkState, StatePassing, ChunkScan kernels) or "single" (the
-    single-pass kernel whenever x is fp16 and no stage tap is requested)."""
+    single-pass kernel whenever x is fp16 and no stage tap other than state_in_q is requested).
+    hand_off_timeouts: an int32 device tensor of one element, or None; receives the number of
+    single-pass waits that ran out (non-zero: the results of the call are not to be used)."""
     _need(x, "x")
     Bsrc, Csrc = (Bq, Cq) if Bq is not None else (B, C)
     B, L, H, P = x.shape
@@ -298,6 +301,8 @@ def ssd_chunk_scan(x: torch.Tensor, dt: torch.Tensor, A: torch.Tensor,
         _need(corr, "corr", torch.float32, (H, P))
     if init_state_q is not None:
         _need(init_state_q, "init_state_q", torch.int8, (B, H, P, N))
+    if hand_off_timeouts is not None:
+        _need(hand_off_timeouts, "hand_off_timeouts", torch.int32, (1,))
     dev = x.device
     y_dtype = x.dtype if y_dtype is None else y_dtype
     if y is None:
@@ -339,6 +344,9 @@ def ssd_chunk_scan(x: torch.Tensor, dt: torch.Tensor, A: torch.Tensor,
     if stage_events is not None:
         a.stage_events = ctypes.cast(stage_events, ctypes.c_void_p)
     a.path = PATHS[path]
+    a.hand_off_timeouts = _ptr(hand_off_timeouts)
+    if hand_off_timeouts is not None:
+        out["hand_off_timeouts"] = hand_off_timeouts
     st = lib().ssdi8_ssd_chunk_scan(ctypes.byref(d), ctypes.byref(a), _stream(stream))
     _check(st, "ssdi8_ssd_chunk_scan")
     return out
@@ -542,11 +550,32 @@ class SSDi8Layer:
         self.dt_softplus, self.decay_shift, self.shift_round = dt_softplus, decay_shift, shift_round
         self.workspace: Optional[torch.Tensor] = None
         self.Bq = self.Cq = None
+        self.timeouts = torch.zeros(1, dtype=torch.int32, device=device)
 
     def __call__(self, x, dt, B, C, *, y=None, taps=(), final_state=True, stage_events=None,
-                 path="auto", quantize_in_bmm=False, stream=None):
+                 path="auto", quantize_in_bmm=False, stream=None, check=True):
         """quantize_in_bmm: hand B, C to ChunkBMM unquantized (one launch fewer per tensor, no
-        row-major int8 copies) instead of quantizing them first with ssdi8_quantize_act."""
+        row-major int8 copies) instead of quantizing them first with ssdi8_quantize_act.
+        check: after the call, wait for the stream and raise if a single-pass hand-off wait ran
+        out (skipped while the stream is being captured into a graph; `hand_off_timeouts()`
+        reads the count of the latest call then)."""
+        out = self._run(x, dt, B, C, y=y, taps=taps, final_state=final_state,
+                        stage_events=stage_events, path=path, quantize_in_bmm=quantize_in_bmm,
+                        stream=stream)
+        capturing = torch.cuda.is_current_stream_capturing()
+        if check and not capturing:
+            n = self.hand_off_timeouts()
+            if n:
+                raise RuntimeError(f"ssdi8_ssd_chunk_scan: {n} single-pass hand-off wait(s) ran "
+                                   "out; y and the final states of this call are unspecified")
+        return out
+
+    def hand_off_timeouts(self) -> int:
+        """Waits that ran out in the latest call (synchronises with the device)."""
+        return int(self.timeouts.item())
+
+    def _run(self, x, dt, B, C, *, y, taps, final_state, stage_events, path, quantize_in_bmm,
+             stream):
         Bt, L, H, P = x.shape
         G = B.shape[2]
         need = workspace_size(dims(Bt, L, H, G))
@@ -559,7 +588,8 @@ class SSDi8Layer:
                                   decay_shift=self.decay_shift, shift_round=self.shift_round,
                                   taps=taps, workspace=self.workspace, y=y,
                                   final_state=final_state, stage_events=stage_events,
-                                  path=path, B=B, C=C, stream=stream)
+                                  path=path, B=B, C=C, stream=stream,
+                                  hand_off_timeouts=self.timeouts)
         if self.Bq is None or self.Bq.shape != B.shape:
             self.Bq = torch.empty(B.shape, dtype=torch.int8, device=x.device)
             self.Cq = torch.empty(C.shape, dtype=torch.int8, device=x.device)
@@ -571,7 +601,7 @@ class SSDi8Layer:
                               decay_shift=self.decay_shift, shift_round=self.shift_round,
                               taps=taps, workspace=self.workspace, y=y,
                               final_state=final_state, stage_events=stage_events,
-                              path=path, stream=stream)
+                              path=path, stream=stream, hand_off_timeouts=self.timeouts)
 
 
 # ------------------------------------------------------------------------------ timing events

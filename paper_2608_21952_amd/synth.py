@@ -134,8 +134,15 @@ def activations(cfg: SSDConfig, stream: int = 1, batch: Optional[int] = None
     B = np.empty((nb, L, G, N), dt_)
     C = np.empty((nb, L, G, N), dt_)
     dt = np.empty((nb, L, H), np.float32)
+    rows = max(1, (1 << 22) // (H * P))   # tokens per block of x (32 MB of fp64 at a time)
     for b in range(nb):
-        x[b] = (g.standard_normal((L, H, P)) * xsc).astype(dt_)
+        # x[b] in consecutive token blocks: the stream yields the same values as one draw of
+        # (L, H, P), without the multi-GB fp64 temporaries
+        for r0 in range(0, L, rows):
+            r1 = min(L, r0 + rows)
+            blk = g.standard_normal((r1 - r0, H, P))
+            blk *= xsc
+            x[b, r0:r1] = blk.astype(dt_)
         B[b] = (g.standard_normal((L, G, N)) * bsc).astype(dt_)
         C[b] = (g.standard_normal((L, G, N)) * csc).astype(dt_)
         dt[b] = g.normal(cfg.dt_mu, cfg.dt_sigma, size=(L, H)).astype(np.float32)

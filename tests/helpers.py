@@ -83,7 +83,8 @@ def run_layer(torch, ssdi8, inp: Dict[str, np.ndarray], sc: Dict[str, np.ndarray
               use_D: bool = True, use_corr: bool = True, y_dtype=None, keep_on_device=False,
               path: str = "auto", workspace=None):
     """Quantize B, C with the static steps (ssdi8_quantize_act) and run ssdi8_ssd_chunk_scan.
-    Returns numpy arrays (or device tensors) of y, final states, Bq, Cq and the taps."""
+    Returns numpy arrays (or device tensors) of y, final states, Bq, Cq, the taps and
+    `hand_off_timeouts` (the count of single-pass waits that ran out)."""
     x = dev(inp["x"], torch)
     dt = dev(inp["dt_raw"], torch)
     B = dev(inp["B"], torch)
@@ -102,7 +103,8 @@ def run_layer(torch, ssdi8, inp: Dict[str, np.ndarray], sc: Dict[str, np.ndarray
         D=f32(inp["D"]) if use_D else None, corr=f32(sc["corr"]) if use_corr else None,
         dt_softplus=dt_softplus, decay_shift=decay_shift, shift_round=shift_round,
         init_state_q=None if init_q is None else dev(init_q, torch), taps=taps,
-        y_dtype=y_dtype, path=path, workspace=workspace)
+        y_dtype=y_dtype, path=path, workspace=workspace,
+        hand_off_timeouts=torch.full((1,), -1, dtype=torch.int32, device="cuda"))
     out["Bq"], out["Cq"] = Bq, Cq
     if c_per_token:
         out["C_scale"] = aC

@@ -231,6 +231,7 @@ def test_scan_argument_errors(ssdi8):
     assert _scan(ssdi8, ok, _scan_args(ssdi8, x_dtype=5)) == ssdi8.ERR_ARG
     assert _scan(ssdi8, ok, _scan_args(ssdi8, x=A16 + 8)) == ssdi8.ERR_ALIGN
     assert _scan(ssdi8, ok, _scan_args(ssdi8, state_q=A16 + 4)) == ssdi8.ERR_ALIGN
+    assert _scan(ssdi8, ok, _scan_args(ssdi8, hand_off_timeouts=A16 + 2)) == ssdi8.ERR_ALIGN
     assert _scan(ssdi8, ok, _scan_args(ssdi8, workspace_bytes=16)) == ssdi8.ERR_WORKSPACE
     assert _scan(ssdi8, ok, _scan_args(ssdi8, workspace=None)) == ssdi8.ERR_WORKSPACE
     ev = (ctypes.c_void_p * 5)(A16, A16, None, A16, A16)
@@ -351,8 +352,12 @@ def test_single_pass_selection(ssdi8):
     assert use(ssdi8.dims(8, 2048, 24, 1), f16, "single")
     assert not use(ssdi8.dims(4, 4096, 80, 1), f16, "separate")
     assert not use(ssdi8.dims(4, 4096, 80, 1), f32, "single")  # fp32 x: separate kernels
-    assert not use(ssdi8.dims(4, 4096, 80, 1), f16, "single", taps=("state_in_q",))
-    assert use(ssdi8.dims(4, 4096, 80, 1), f16, "single", taps=("cb_q",))   # ChunkBMM taps ok
+    assert not use(ssdi8.dims(4, 4096, 80, 1), f16, "single", taps=("state_q",))
+    assert not use(ssdi8.dims(4, 4096, 80, 1), f16, "single", taps=("dt_post",))
+    # ChunkBMM's taps and the entering states are available from the single pass
+    assert use(ssdi8.dims(4, 4096, 80, 1), f16, "single", taps=("cb_q",))
+    assert use(ssdi8.dims(4, 4096, 80, 1), f16, "single", taps=("state_in_q",))
+    assert use(ssdi8.dims(4, 4096, 80, 1), f16, taps=("state_in_q",))
     assert not use(ssdi8.dims(4, 300, 80, 1), f16, "single")   # invalid sizes
 
 

@@ -191,11 +191,16 @@ def test_layer_wide_dt_range(torch, ssdi8):
     for b in range(cfg.batch):
         for h in range(cfg.nheads):
             check_slab(g, inp, sc, b, h, cfg.chunk, out_dtype=np.float32)
-    one = run_layer(torch, ssdi8, inp, sc, path="single", y_dtype=torch.float32)
+    one = run_layer(torch, ssdi8, inp, sc, path="single", y_dtype=torch.float32,
+                    taps=("state_in_q",))
+    assert int(one["hand_off_timeouts"][0]) == 0
     ref = oq.ssdi8_forward(inp["x"], inp["dt_raw"], inp["A"], inp["B"], inp["C"], inp["D"],
-                           sc["corr"], sc, chunk=cfg.chunk, want=("y64", "final_q"))
+                           sc["corr"], sc, chunk=cfg.chunk, want=("y64", "final_q", "pin"))
     assert np.isfinite(ref["y64"]).all()
+    assert_equal(one["state_in_q"], g["state_in_q"], "P_in single pass vs separate (wide dt)")
+    assert_equal(one["state_in_q"], ref["pin"], "P_in single pass vs oracle (wide dt)")
     assert np.array_equal(one["final_state_q"], ref["final_q"])
+    assert_equal(one["y"], g["y"], "y single pass vs separate kernels (wide dt)")
     assert_close(one["y"], ref["y64"], "y (single pass, wide dt)")
 
 
