@@ -293,6 +293,7 @@ ssdi8_status ssdi8_ssd_chunk_scan(const ssdi8_dims* d, const ssdi8_scan_args* a,
     if (!mark(2) || !mark(3)) return SSDI8_ERR_HIP;
     ssdi8::FusedState fs;
     fs.bqT = bqT;
+    fs.sq = sq;
     fs.B_scale = a->B_scale;
     fs.xs_scale = a->xs_scale;
     fs.xs_per_head = a->xs_per_head;

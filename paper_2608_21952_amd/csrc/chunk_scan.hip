@@ -37,6 +37,11 @@ static_assert(kP * kXTS >= kQ * kP * 2, "the fp16 output stage reuses the x^T by
 // A diagonal block whose decay span r_{J-1} - r_J stays below this bound forms its weights as
 // (a_CB dt_i exp(-(cs_i - r_{J-1}))) * exp(cs_j - r_{J-1}) without overflow in fp32.
 constexpr float kDiagSpan = 64.0f;
+// Single pass: how many earlier chunks a chunk looks back over for a published entering state,
+// and the status bits of a chunk's flag word (its Q(Decay) in the low 16 bits).
+constexpr int kLook = 4;
+constexpr uint32_t kFlagS = 1u << 16;   // the chunk-local S_q of the chunk is published
+constexpr uint32_t kFlagP = 1u << 17;   // the state entering the next chunk is published
 
 // Two adjacent channels of one token row, loaded raw and converted to fp16 for the MFMA.
 template <typename XT> struct Pair;
@@ -89,7 +94,8 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
     float cr[kP];
     double r[8];         // r_t: cs at the last token of block t
     double scan[4];
-    int misc[4];         // single pass: ticket, q_d
+    int misc[4];         // single pass: ticket, q_d, look-back anchor
+    int lq[kLook];       // single pass: Q(Decay) of chunks c-1, c-2, ... (flag words' low half)
     // x^T [p][i] fp16: the ChunkScan2 MFMA operand and, for fp16 x, the D skip operand; then
     // the stage of the fp16 output (256 rows of 128 bytes).
     uint8_t xT[kP * kXTS];
@@ -301,83 +307,184 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
     __syncthreads();
   }
 
-  // ---- single pass, StatePassing (Eq. 9) for this chunk: wait until the previous chunk of the
-  //      sequence has published P_in[c] (bounded: a wait that runs out is counted in the
-  //      wait counter sync[kSyncWait] and the kernel still finishes), then
-  //      P_in[c+1] = clamp(S_q + ((q_d P_in[c] + r) >> k)), published with agent-coherent
-  //      stores before the flag.  Every lane updates its own 32 state bytes in registers.
+  // ---- single pass, StatePassing (Eq. 9) for this chunk.  P_in[c], the state entering the
+  //      chunk, comes from the chunks before it in its sequence.  The flag word of chunk m holds
+  //      its Q(Decay) in the low 16 bits and two status bits: kFlagS (its chunk-local S_q is in
+  //      the sq slot of (b, m, h)) and kFlagP (P_in[m+1] is in the pin slot of (b, m+1, h)).
+  //      With kFlagP at chunk c-1-l (l < kLook) and kFlagS on every chunk in between,
+  //      P_in[c] = Eq. 9 applied to P_in[c-l] over the S_q of chunks c-l, ..., c-1 in chunk order:
+  //      the same recurrence, hence the same integers as a chain of hand-offs from chunk to
+  //      chunk, without waiting for each of them.  A chunk that finds no such anchor at its first
+  //      look publishes its own S_q (so that later chunks can look past it), then polls until it
+  //      does; every chunk then publishes P_in[c+1].  Only earlier chunks of the same sequence
+  //      are waited for; they hold earlier tickets of the same counter, so each is running or
+  //      done, publishes its S_q before it waits, and chunk 0 waits for nothing.  Waits are
+  //      bounded: one that runs out is counted (sync[kSyncWait] and the caller's counter) and the
+  //      kernel still finishes.  Each lane updates its own 32 state bytes in registers; payloads
+  //      are written and read at the agent's coherence point (sc1) and are complete before
+  //      their flag is set.
   auto hand_off = [&]() {
+    constexpr size_t kSlab = (size_t)kP * kN;
+    constexpr int kPolicySc1 = 16;
     const int bh = b * H + h;
-    int* flags = fs.sync + kSyncFlags;
-    if (c > 0 && t == 0) {
-      const int* f = flags + (size_t)bh * nc + (c - 1);
-      int ok = 0;
-      for (int it = 0; it < fs.spin_limit; ++it) {
-        if (__hip_atomic_load(f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) {
-          ok = 1;
-          break;
-        }
-        __builtin_amdgcn_s_sleep(2);
+    int* flags = fs.sync + kSyncFlags + (size_t)bh * nc;   // flag of chunk m at flags[m]
+    const int qd = sm.misc[1];
+    auto slab_of = [&](int8_t* base, int cc) {
+      return base + (((size_t)b * nc + cc) * H + h) * kSlab;
+    };
+    // this lane's 16-byte slices of the two state tiles of a slab
+    const uint32_t off0 = (uint32_t)((mt * (kN / 32) + ntb) * 1024 + lane * 16);
+    const uint32_t off1 = off0 + 1024;
+    auto ld_sc1 = [&](const int8_t* slab, uint32_t off) {
+      const auto v = __builtin_amdgcn_raw_buffer_load_b128(buffer_rsrc(slab), (int)off, 0,
+                                                           kPolicySc1);
+      return make_uint4(v[0], v[1], v[2], v[3]);
+    };
+    auto st_sc1 = [&](uint4 d, int8_t* slab, uint32_t off) {
+      typedef uint32_t u32x4 __attribute__((vector_size(16)));
+      const u32x4 v = {d.x, d.y, d.z, d.w};
+      __builtin_amdgcn_raw_buffer_store_b128(v, buffer_rsrc(slab), (int)off, 0, kPolicySc1);
+    };
+    // Eq. 9 on the 32 bytes of a lane: state st, chunk-local s, Q(Decay) q
+    auto step = [&](uint4 st, uint4 sl, int q) {
+      const uint32_t a[4] = {st.x, st.y, st.z, st.w}, sv[4] = {sl.x, sl.y, sl.z, sl.w};
+      uint32_t o[4];
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4) {
+        int v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          v[e] = pass_step(sext8(a[g4], e), sext8(sv[g4], e), q, fs.shift, fs.radd);
+        o[g4] = pack4_i8(v[0], v[1], v[2], v[3]);
       }
-      if (!ok) {
-        atomicAdd(fs.sync + kSyncWait, 1);
-        if (fs.timeouts) atomicAdd(fs.timeouts, 1);
-      }
-    }
-    __syncthreads();
-    {
-      constexpr size_t kSlab = (size_t)kP * kN;
-      const int qd = sm.misc[1];
-      int8_t* slab = pin + (((size_t)b * nc + c) * H + h) * kSlab;
+      return make_uint4(o[0], o[1], o[2], o[3]);
+    };
+    // wave 0: the flags of chunks c-1-lane (lane < kLook); the nearest anchor lane l, or -1
+    auto look = [&](uint32_t* fout) {
+      const int m = c - 1 - lane;
+      uint32_t f = 0;
+      if (lane < kLook && m >= 0)
+        f = (uint32_t)__hip_atomic_load(flags + m, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      *fout = f;
+      const uint64_t mp = __ballot((f & kFlagP) != 0);
+      const uint64_t ma = __ballot((f & (kFlagS | kFlagP)) != 0);
+      const int lp = mp ? (int)__builtin_ctzll(mp) : 64;
+      const int la = (int)__builtin_ctzll(~ma);   // lanes >= kLook never hold a status
+      return (lp < kLook && la >= lp) ? lp : -1;
+    };
+    const uint4 sq0 = make_uint4(sq[0][0], sq[0][1], sq[0][2], sq[0][3]);
+    const uint4 sq1 = make_uint4(sq[1][0], sq[1][1], sq[1][2], sq[1][3]);
+    uint4 p0, p1;   // P_in[c]
+    if (c == 0) {
+      // the initial state (row-major; 0 without one), also ChunkScan1's entering state of chunk 0
+      uint32_t w[2][4];
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
-        const uint32_t off = (uint32_t)((mt * (kN / 32) + ntb + i) * 1024 + lane * 16);
         // row-major (p, n) of this lane's byte 4 g + e: p = prow, n = 32 (ntb + i) + 8 g + 4 hf + e
         const size_t rbase = (size_t)bh * kSlab + (size_t)prow * kN + 32 * (ntb + i) + 4 * hf;
-        uint32_t cw[4];
-        if (c > 0) {
-          // sc1: read at the agent's coherence point (written there by the publisher)
-          const auto v = __builtin_amdgcn_raw_buffer_load_b128(buffer_rsrc(slab), (int)off, 0, 16);
-          cw[0] = v[0]; cw[1] = v[1]; cw[2] = v[2]; cw[3] = v[3];
-        } else {
 #pragma unroll
-          for (int g4 = 0; g4 < 4; ++g4)
-            cw[g4] = fs.init ? *reinterpret_cast<const uint32_t*>(fs.init + rbase + 8 * g4) : 0u;
-          // the entering state of the first chunk, in the order ChunkScan1 reads it
-          *reinterpret_cast<uint4*>(slab + off) = make_uint4(cw[0], cw[1], cw[2], cw[3]);
-        }
-        uint32_t nw[4];
-#pragma unroll
-        for (int g4 = 0; g4 < 4; ++g4) {
-          int v[4];
-#pragma unroll
-          for (int e = 0; e < 4; ++e)
-            v[e] = pass_step(sext8(cw[g4], e), sext8(sq[i][g4], e), qd, fs.shift, fs.radd);
-          nw[g4] = pack4_i8(v[0], v[1], v[2], v[3]);
-        }
-        if (c + 1 < nc) {
-          typedef uint32_t u32x4 __attribute__((vector_size(16)));
-          const u32x4 v = {nw[0], nw[1], nw[2], nw[3]};
-          // sc1: written through to the agent's coherence point
-          __builtin_amdgcn_raw_buffer_store_b128(v, buffer_rsrc(slab + kSlab * H), (int)off, 0,
-                                                 16);
-        } else {
-          const float a = state_scale[h * kP + prow];
-#pragma unroll
-          for (int g4 = 0; g4 < 4; ++g4) {
-            if (fs.final_q) *reinterpret_cast<uint32_t*>(fs.final_q + rbase + 8 * g4) = nw[g4];
-            if (fs.final_state)
-              *reinterpret_cast<float4*>(fs.final_state + rbase + 8 * g4) =
-                  make_float4((float)sext8(nw[g4], 0) * a, (float)sext8(nw[g4], 1) * a,
-                              (float)sext8(nw[g4], 2) * a, (float)sext8(nw[g4], 3) * a);
+        for (int g4 = 0; g4 < 4; ++g4)
+          w[i][g4] = fs.init ? *reinterpret_cast<const uint32_t*>(fs.init + rbase + 8 * g4) : 0u;
+      }
+      p0 = make_uint4(w[0][0], w[0][1], w[0][2], w[0][3]);
+      p1 = make_uint4(w[1][0], w[1][1], w[1][2], w[1][3]);
+      int8_t* slab = slab_of(pin, 0);
+      *reinterpret_cast<uint4*>(slab + off0) = p0;
+      *reinterpret_cast<uint4*>(slab + off1) = p1;
+    } else {
+      if (wv == 0) {
+        uint32_t f;
+        const int l = look(&f);
+        if (lane == 0) sm.misc[2] = l;
+        if (lane < kLook) sm.lq[lane] = (int)(f & 0xffffu);
+      }
+      __syncthreads();
+      int l = __builtin_amdgcn_readfirstlane(sm.misc[2]);
+      if (l < 0) {
+        // publish S_q[c] for the chunks after this one, then wait for an anchor
+        int8_t* sslab = slab_of(fs.sq, c);
+        st_sc1(sq0, sslab, off0);
+        st_sc1(sq1, sslab, off1);
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+        if (wv == 0) {
+          if (lane == 0)
+            __hip_atomic_store(flags + c, (int)(kFlagS | (uint32_t)qd), __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+          uint32_t f = 0;
+          int found = -1;
+          for (int it = 0; it < fs.spin_limit && found < 0; ++it) {
+            __builtin_amdgcn_s_sleep(2);
+            found = look(&f);
           }
+          if (found < 0) {
+            if (lane == 0) {
+              atomicAdd(fs.sync + kSyncWait, 1);
+              if (fs.timeouts) atomicAdd(fs.timeouts, 1);
+            }
+            found = 0;
+          }
+          if (lane == 0) sm.misc[2] = found;
+          if (lane < kLook) sm.lq[lane] = (int)(f & 0xffffu);
+        }
+        __syncthreads();
+        l = __builtin_amdgcn_readfirstlane(sm.misc[2]);
+      }
+      // P_in[c-l] (published by the anchor chunk c-1-l) and the S_q of chunks c-l .. c-1, all
+      // loads in flight together
+      const int8_t* pslab = slab_of(pin, c - l);
+      p0 = ld_sc1(pslab, off0);
+      p1 = ld_sc1(pslab, off1);
+      uint4 s0[kLook - 1], s1[kLook - 1];
+#pragma unroll
+      for (int k = 0; k < kLook - 1; ++k) {
+        if (k < l) {
+          const int8_t* sslab = slab_of(fs.sq, c - l + k);
+          s0[k] = ld_sc1(sslab, off0);
+          s1[k] = ld_sc1(sslab, off1);
         }
       }
-      __builtin_amdgcn_s_waitcnt(0);
+#pragma unroll
+      for (int k = 0; k < kLook - 1; ++k) {
+        if (k < l) {
+          const int qk = sm.lq[l - 1 - k];   // Q(Decay) of chunk c - l + k
+          p0 = step(p0, s0[k], qk);
+          p1 = step(p1, s1[k], qk);
+        }
+      }
+      if (l > 0) {
+        // ChunkScan1 reads the entering state from the pin slot of this chunk
+        int8_t* slab = slab_of(pin, c);
+        st_sc1(p0, slab, off0);
+        st_sc1(p1, slab, off1);
+      }
     }
+    // P_in[c+1] = clamp(S_q[c] + ((q_d P_in[c] + r) >> k))
+    const uint4 n0 = step(p0, sq0, qd), n1 = step(p1, sq1, qd);
+    if (c + 1 < nc) {
+      int8_t* slab = slab_of(pin, c + 1);
+      st_sc1(n0, slab, off0);
+      st_sc1(n1, slab, off1);
+    } else {
+      const float a = state_scale[h * kP + prow];
+      const uint32_t nw[2][4] = {{n0.x, n0.y, n0.z, n0.w}, {n1.x, n1.y, n1.z, n1.w}};
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const size_t rbase = (size_t)bh * kSlab + (size_t)prow * kN + 32 * (ntb + i) + 4 * hf;
+#pragma unroll
+        for (int g4 = 0; g4 < 4; ++g4) {
+          if (fs.final_q) *reinterpret_cast<uint32_t*>(fs.final_q + rbase + 8 * g4) = nw[i][g4];
+          if (fs.final_state)
+            *reinterpret_cast<float4*>(fs.final_state + rbase + 8 * g4) =
+                make_float4((float)sext8(nw[i][g4], 0) * a, (float)sext8(nw[i][g4], 1) * a,
+                            (float)sext8(nw[i][g4], 2) * a, (float)sext8(nw[i][g4], 3) * a);
+        }
+      }
+    }
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (t == 0 && c + 1 < nc)
-      __hip_atomic_store(flags + (size_t)bh * nc + c, 1, __ATOMIC_RELAXED,
+      __hip_atomic_store(flags + c, (int)(kFlagP | (uint32_t)qd), __ATOMIC_RELAXED,
                          __HIP_MEMORY_SCOPE_AGENT);
   };
 

@@ -62,13 +62,14 @@ hipError_t launch_chunk_scan(const LayerDims& d, const void* x, int x_dtype, con
                              int32_t* y1_tap, hipStream_t st);
 
 // Single pass of ChunkState, StatePassing and ChunkScan (fp16 x): one workgroup per (b, c, h)
-// in ticket order; each computes its chunk's S_q, waits for the previous chunk of its sequence
-// to publish P_in[c] (pin slot c, permuted kslice order, as C_q), publishes P_in[c+1] (slot
-// c + 1, or the final states) and runs ChunkScan1/2 with x still in LDS.  sync (int words,
-// cleared beforehand by ChunkBMM): the ticket counter of sequence class x at x * kSyncLine (one
-// 128-byte line each, so that the classes' atomics do not serialize on one line), the count of
-// waits that ran out at kSyncWait, and from kSyncFlags + (b H + h) nc + c the flag "slot c + 1
-// published".
+// in ticket order; each computes its chunk's S_q, obtains P_in[c] from the chunks before it (the
+// previous chunk's P_in[c] in pin slot c, or an earlier published entering state and the
+// published S_q of the chunks in between, sq slots; permuted kslice order, as C_q), publishes
+// P_in[c+1] (slot c + 1, or the final states) and runs ChunkScan1/2 with x still in LDS.  sync
+// (int words, cleared beforehand by ChunkBMM): the ticket counter of sequence class x at
+// x * kSyncLine (one 128-byte line each, so that the classes' atomics do not serialize on one
+// line), the count of waits that ran out at kSyncWait, and from kSyncFlags + (b H + h) nc + c
+// the flag word of chunk c (its Q(Decay) and whether its S_q and P_in[c+1] are published).
 constexpr int kSyncLine = 32;
 constexpr int kSyncMaxClasses = 64;
 constexpr int kSyncWait = kSyncMaxClasses * kSyncLine;
@@ -82,6 +83,7 @@ inline int sync_classes(int nbh) {
 }
 struct FusedState {
   const int8_t* bqT = nullptr;
+  int8_t* sq = nullptr;      // published chunk-local states, one P x N slab per (b, c, h)
   const float* B_scale = nullptr;
   const float* xs_scale = nullptr;
   int xs_per_head = 0;
