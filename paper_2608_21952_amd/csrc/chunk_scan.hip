@@ -345,17 +345,26 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
       const u32x4 v = {d.x, d.y, d.z, d.w};
       __builtin_amdgcn_raw_buffer_store_b128(v, buffer_rsrc(slab), (int)off, 0, kPolicySc1);
     };
-    // Eq. 9 on the 32 bytes of a lane: state st, chunk-local s, Q(Decay) q
+    // Eq. 9 on the 32 bytes of a lane: state st, chunk-local s, Q(Decay) q (packed 16-bit
+    // arithmetic for shifts up to 8 and 0 <= q <= 2^shift, where it is exact; 32-bit
+    // otherwise, e.g. for a decay above 1 from inputs outside the method's domain)
     auto step = [&](uint4 st, uint4 sl, int q) {
       const uint32_t a[4] = {st.x, st.y, st.z, st.w}, sv[4] = {sl.x, sl.y, sl.z, sl.w};
       uint32_t o[4];
+      if (fs.shift <= 8 && q >= 0 && q <= (1 << fs.shift)) {
+        const s16x2 q2 = {(short)q, (short)q}, r2 = {(short)fs.radd, (short)fs.radd};
+        const s16x2 k2 = {(short)fs.shift, (short)fs.shift};
 #pragma unroll
-      for (int g4 = 0; g4 < 4; ++g4) {
-        int v[4];
+        for (int g4 = 0; g4 < 4; ++g4) o[g4] = pass_step4_pk16(a[g4], sv[g4], q2, r2, k2);
+      } else {
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
-          v[e] = pass_step(sext8(a[g4], e), sext8(sv[g4], e), q, fs.shift, fs.radd);
-        o[g4] = pack4_i8(v[0], v[1], v[2], v[3]);
+        for (int g4 = 0; g4 < 4; ++g4) {
+          int v[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            v[e] = pass_step(sext8(a[g4], e), sext8(sv[g4], e), q, fs.shift, fs.radd);
+          o[g4] = pack4_i8(v[0], v[1], v[2], v[3]);
+        }
       }
       return make_uint4(o[0], o[1], o[2], o[3]);
     };
@@ -466,7 +475,7 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
       st_sc1(n0, slab, off0);
       st_sc1(n1, slab, off1);
     } else {
-      const float a = state_scale[h * kP + prow];
+      const float a = s_aS[prow];   // state_scale[h, prow], staged in LDS at the start
       const uint32_t nw[2][4] = {{n0.x, n0.y, n0.z, n0.w}, {n1.x, n1.y, n1.z, n1.w}};
 #pragma unroll
       for (int i = 0; i < 2; ++i) {

@@ -78,6 +78,30 @@ __device__ __forceinline__ int pass_step(int s, int add, int q, int shift, int r
   return v < -kQMax ? -kQMax : (v > kQMax ? kQMax : v);
 }
 
+// The same step on the four int8 elements of a dword pair (state word p, chunk-local word s),
+// two elements per packed 16-bit instruction.  Valid for shift <= 8 with 0 <= q <= 2^shift:
+// |q P + r| <= 256 * 127 + 128 < 2^15, so every value fits an int16 and the packed arithmetic
+// is exact.  Bytes are sign-extended by a left shift of the dword and arithmetic right shifts
+// of its halves (even bytes: (w << 8) >> 8 per half; odd bytes: w >> 8 per half), and the
+// results are gathered back with one byte permute.
+typedef short s16x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pass_step4_pk16(uint32_t p, uint32_t s, s16x2 q, s16x2 r,
+                                                    s16x2 shift) {
+  const s16x2 eight = {8, 8};
+  const s16x2 pe = __builtin_bit_cast(s16x2, p << 8) >> eight;
+  const s16x2 po = __builtin_bit_cast(s16x2, p) >> eight;
+  const s16x2 se = __builtin_bit_cast(s16x2, s << 8) >> eight;
+  const s16x2 so = __builtin_bit_cast(s16x2, s) >> eight;
+  const s16x2 lo = {-kQMax, -kQMax}, hi = {kQMax, kQMax};
+  s16x2 ve = se + ((q * pe + r) >> shift);
+  s16x2 vo = so + ((q * po + r) >> shift);
+  ve = __builtin_elementwise_max(__builtin_elementwise_min(ve, hi), lo);
+  vo = __builtin_elementwise_max(__builtin_elementwise_min(vo, hi), lo);
+  // bytes (ve.x, vo.x, ve.y, vo.y)
+  return __builtin_amdgcn_perm(__builtin_bit_cast(uint32_t, vo), __builtin_bit_cast(uint32_t, ve),
+                               0x06020400u);
+}
+
 // The low bytes of four words in one dword (byte i = low byte of w_i): two byte permutes and a
 // shift-or.
 __device__ __forceinline__ uint32_t pack_lo4(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3) {
