@@ -160,6 +160,59 @@ __global__ __launch_bounds__(256) void absmax_granules(const T* __restrict__ src
     if (smax[i]) atomicMax(&acc[i], smax[i]);
 }
 
+// The same absmax when the k m values of a (b, l) row split into 16-byte units of kE elements
+// that never straddle two granules (m % kE == 0): the rows are the outer loop and each thread
+// owns fixed units (columns) of them, so the granule of each of its values never changes and
+// its running maxima stay in registers (kE of them per column for CHANNEL, one otherwise).
+// A block is TR rows x TC columns of threads; LDS atomics only when a thread leaves a column.
+template <typename T>
+__global__ __launch_bounds__(256) void absmax_cols(const T* __restrict__ src,
+                                                   uint32_t* __restrict__ acc, int gran,
+                                                   int64_t rows, int cols, int tc, int m,
+                                                   int ngran) {
+  constexpr int kE = 16 / sizeof(T);
+  __shared__ uint32_t smax[kMaxGranules];
+  for (int i = threadIdx.x; i < ngran; i += blockDim.x) smax[i] = 0u;
+  __syncthreads();
+  const int tx = threadIdx.x % tc, ty = threadIdx.x / tc, tr = blockDim.x / tc;
+  for (int col = tx; col < cols; col += tc) {
+    float mx[kE];
+#pragma unroll
+    for (int e = 0; e < kE; ++e) mx[e] = 0.0f;
+    for (int64_t row = (int64_t)blockIdx.x * tr + ty; row < rows; row += (int64_t)gridDim.x * tr) {
+      const uint4 u = reinterpret_cast<const uint4*>(src + (row * cols + col) * kE)[0];
+      if constexpr (sizeof(T) == 2) {
+        const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+        for (int e = 0; e < kE; ++e) {
+          const float v = (float)__builtin_bit_cast(
+              _Float16, (uint16_t)((e & 1) ? (w[e >> 1] >> 16) : (w[e >> 1] & 0xffffu)));
+          mx[e] = __builtin_fmaxf(mx[e], __builtin_fabsf(v));
+        }
+      } else {
+        const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+        for (int e = 0; e < kE; ++e)
+          mx[e] = __builtin_fmaxf(mx[e], __builtin_fabsf(__uint_as_float(w[e])));
+      }
+    }
+    if (gran == 2) {
+#pragma unroll
+      for (int e = 0; e < kE; ++e)
+        if (mx[e] > 0.0f) atomicMax(&smax[col * kE + e], __float_as_uint(mx[e]));
+    } else {
+      float v = mx[0];
+#pragma unroll
+      for (int e = 1; e < kE; ++e) v = __builtin_fmaxf(v, mx[e]);
+      const int gi = gran == 0 ? 0 : (col * kE) / m;
+      if (v > 0.0f) atomicMax(&smax[gi], __float_as_uint(v));
+    }
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < ngran; i += blockDim.x)
+    if (smax[i]) atomicMax(&acc[i], smax[i]);
+}
+
 __global__ void absmax_to_step(float* scale, int n) {
   int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n) {
@@ -209,7 +262,17 @@ hipError_t quantize_impl(const T* src, int64_t b, int64_t l, int64_t k, int64_t 
     const int ngran = gran == 0 ? 1 : (gran == 1 ? (int)k : (int)(k * m));
     hipLaunchKernelGGL(fill_u32, dim3((unsigned)grid_for(ngran)), dim3(256), 0, st,
                        reinterpret_cast<uint32_t*>(scale), (int64_t)ngran, 0u);
-    if (n > 0) {
+    constexpr int kE = 16 / sizeof(T);
+    const int64_t cols = k * m / kE;
+    if (n > 0 && m % kE == 0 && cols <= ((int64_t)1 << 20)) {
+      // columns of 16-byte units, rows of b l: a wave spans up to 64 consecutive units of a row
+      const int tc = cols < 64 ? (int)cols : 64;
+      const int tr = 256 / tc;
+      const int64_t rows = b * l;
+      hipLaunchKernelGGL(absmax_cols<T>, dim3((unsigned)grid_for(rows, tr, 2048)), dim3(256), 0,
+                         st, src, reinterpret_cast<uint32_t*>(scale), gran, rows, (int)cols, tc,
+                         (int)m, ngran);
+    } else if (n > 0) {
       hipLaunchKernelGGL(absmax_granules<T>, dim3((unsigned)grid_for(n, 256, 2048)), dim3(256),
                          0, st, src, reinterpret_cast<uint32_t*>(scale), gran, n, k, m, ngran);
     }
