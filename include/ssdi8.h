@@ -203,6 +203,24 @@ size_t ssdi8_ssd_workspace_size(const ssdi8_dims* d);
  */
 ssdi8_status ssdi8_ssd_chunk_scan(const ssdi8_dims* d, const ssdi8_scan_args* a, void* stream);
 
+/*
+ * ssdi8_ssd_chunk_scan_noalloc — ssdi8_ssd_chunk_scan for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same arguments and results, with `workspace` NULL and `workspace_bytes` 0; the scratch is
+ * the library's own static device array of 128 MiB (134217728 bytes), one per GPU, created with
+ * the library's device code and held until the process ends.  The call allocates nothing; its
+ * first call on a device looks up that device's copy of the array.
+ * Limit: ssdi8_ssd_workspace_size(d) must not exceed 128 MiB (e.g. 65536 tokens x 24 heads,
+ * 16384 tokens x 80 heads); larger sizes return SSDI8_ERR_WORKSPACE before anything is launched.
+ * A non-NULL workspace returns SSDI8_ERR_ARG.
+ * Every call on one GPU uses the same scratch: calls that overlap on a GPU (on different streams,
+ * or from different threads without ordering) race and give unspecified results; calls ordered
+ * on one stream are safe (each call clears what must start at zero without hipMemsetAsync, so it
+ * can be captured in a graph).
+ */
+ssdi8_status ssdi8_ssd_chunk_scan_noalloc(const ssdi8_dims* d, const ssdi8_scan_args* a,
+                                          void* stream);
+
 /* 1 if ssdi8_ssd_chunk_scan with these arguments runs the single-pass kernel (see `path`), 0 if
    the separate kernels (or on invalid sizes).  Host only; launches nothing. */
 int ssdi8_uses_single_pass(const ssdi8_dims* d, const ssdi8_scan_args* a);

@@ -4,11 +4,41 @@
 
 #include <hip/hip_runtime.h>
 
+#include <mutex>
+
 #include "common.hpp"
 #include "frag.hpp"
 #include "launch.hpp"
 
+// Scratch of ssdi8_ssd_chunk_scan_noalloc: the workspace of a call that brings none.  One copy
+// per GPU, held until the process ends; calls on one GPU share it.
+constexpr size_t kNoAllocScratchBytes = (size_t)128 << 20;
+static __device__ __attribute__((aligned(256))) unsigned char scratch[kNoAllocScratchBytes];
+
 namespace {
+
+// The device address of `scratch` on the current device, looked up once per device (host code
+// must never pass the array's own name to a kernel: on the host it is a stand-in, not a device
+// address).
+constexpr int kMaxDevices = 64;
+std::once_flag g_scratch_once[kMaxDevices];
+void* g_scratch_ptr[kMaxDevices];
+hipError_t g_scratch_err[kMaxDevices];
+
+hipError_t scratch_address(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::call_once(g_scratch_once[dev], [dev]() {
+    void* p = nullptr;
+    g_scratch_err[dev] = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    g_scratch_ptr[dev] = p;
+  });
+  if (g_scratch_err[dev] != hipSuccess) return g_scratch_err[dev];
+  *out = g_scratch_ptr[dev];
+  return *out ? hipSuccess : hipErrorInvalidSymbol;
+}
 
 using ssdi8::LayerDims;
 
@@ -334,6 +364,23 @@ ssdi8_status ssdi8_ssd_chunk_scan(const ssdi8_dims* d, const ssdi8_scan_args* a,
                                a->D, a->corr, a->y, a->y_dtype, a->scan1_i32, st);
   if (e != hipSuccess || !mark(4)) return SSDI8_ERR_HIP;
   return SSDI8_OK;
+}
+
+ssdi8_status ssdi8_ssd_chunk_scan_noalloc(const ssdi8_dims* d, const ssdi8_scan_args* a,
+                                          void* stream) {
+  ssdi8_status s = check_dims(d);
+  if (s != SSDI8_OK) return s;
+  if (!a) return SSDI8_ERR_NULL;
+  if (a->workspace || a->workspace_bytes) return SSDI8_ERR_ARG;
+  if (plan_workspace(d).total > kNoAllocScratchBytes) return SSDI8_ERR_WORKSPACE;
+  ssdi8_scan_args b = *a;
+  if (d->batch > 0 && d->seqlen > 0) {
+    void* ws = nullptr;
+    if (scratch_address(&ws) != hipSuccess) return SSDI8_ERR_HIP;
+    b.workspace = ws;
+    b.workspace_bytes = kNoAllocScratchBytes;
+  }
+  return ssdi8_ssd_chunk_scan(d, &b, stream);
 }
 
 size_t ssdi8_fp16_workspace_size(const ssdi8_dims* d) {

@@ -107,6 +107,9 @@ def lib() -> ctypes.CDLL:
     L.ssdi8_ssd_workspace_size.restype = ctypes.c_size_t
     L.ssdi8_ssd_chunk_scan.argtypes = [ctypes.POINTER(Dims), ctypes.POINTER(ScanArgs), _P]
     L.ssdi8_ssd_chunk_scan.restype = _I
+    L.ssdi8_ssd_chunk_scan_noalloc.argtypes = [ctypes.POINTER(Dims), ctypes.POINTER(ScanArgs),
+                                               _P]
+    L.ssdi8_ssd_chunk_scan_noalloc.restype = _I
     L.ssdi8_uses_single_pass.argtypes = [ctypes.POINTER(Dims), ctypes.POINTER(ScanArgs)]
     L.ssdi8_uses_single_pass.restype = _I
     L.ssdi8_decode_step.argtypes = [i64, i64, i64, i64, i64, ctypes.POINTER(DecodeArgs), _P]
@@ -262,7 +265,8 @@ def ssd_chunk_scan(x: torch.Tensor, dt: torch.Tensor, A: torch.Tensor,
                    y: Optional[torch.Tensor] = None, stage_events=None,
                    path: str = "auto", B: Optional[torch.Tensor] = None,
                    C: Optional[torch.Tensor] = None, stream=None,
-                   hand_off_timeouts: Optional[torch.Tensor] = None) -> Dict[str, torch.Tensor]:
+                   hand_off_timeouts: Optional[torch.Tensor] = None,
+                   _noalloc: bool = False) -> Dict[str, torch.Tensor]:
     """One SSDi8 SSD layer (ssdi8_ssd_chunk_scan).  Shapes: x (B,L,H,P), dt (B,L,H), A (H),
     Bq/Cq (B,L,G,N) int8 -- or Bq = Cq = None and B, C (B,L,G,N) fp16/fp32 unquantized, then
     quantized with the static B_scale, C_scale inside ChunkBMM --, B_scale (G), C_scale (G) or
@@ -309,10 +313,13 @@ def ssd_chunk_scan(x: torch.Tensor, dt: torch.Tensor, A: torch.Tensor,
         y = torch.empty((B, L, H, P), dtype=y_dtype, device=dev)
     _need(y, "y", y_dtype, (B, L, H, P))
     d = dims(B, L, H, G, P, N, chunk)
-    need = workspace_size(d)
-    if workspace is None:
-        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
-    _need(workspace, "workspace", torch.uint8)
+    if not _noalloc:
+        need = workspace_size(d)
+        if workspace is None:
+            workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+        _need(workspace, "workspace", torch.uint8)
+    elif workspace is not None:
+        raise ValueError("ssd_chunk_scan_noalloc takes no workspace")
     a = ScanArgs()
     a.x, a.x_dtype = _ptr(x), _fdt(x)
     a.dt, a.dt_softplus, a.A = _ptr(dt), int(dt_softplus), _ptr(A)
@@ -340,16 +347,31 @@ def ssd_chunk_scan(x: torch.Tensor, dt: torch.Tensor, A: torch.Tensor,
         t = torch.zeros(shp(B, L, H, P, G, N, chunk, c), dtype=dty, device=dev)
         out[name] = t
         setattr(a, name, _ptr(t))
-    a.workspace, a.workspace_bytes = _ptr(workspace), workspace.numel()
+    if workspace is not None:
+        a.workspace, a.workspace_bytes = _ptr(workspace), workspace.numel()
     if stage_events is not None:
         a.stage_events = ctypes.cast(stage_events, ctypes.c_void_p)
     a.path = PATHS[path]
     a.hand_off_timeouts = _ptr(hand_off_timeouts)
     if hand_off_timeouts is not None:
         out["hand_off_timeouts"] = hand_off_timeouts
-    st = lib().ssdi8_ssd_chunk_scan(ctypes.byref(d), ctypes.byref(a), _stream(stream))
-    _check(st, "ssdi8_ssd_chunk_scan")
+    if _noalloc:
+        st = lib().ssdi8_ssd_chunk_scan_noalloc(ctypes.byref(d), ctypes.byref(a), _stream(stream))
+        _check(st, "ssdi8_ssd_chunk_scan_noalloc")
+    else:
+        st = lib().ssdi8_ssd_chunk_scan(ctypes.byref(d), ctypes.byref(a), _stream(stream))
+        _check(st, "ssdi8_ssd_chunk_scan")
     return out
+
+
+def ssd_chunk_scan_noalloc(*args, **kw) -> Dict[str, torch.Tensor]:
+    """ssdi8_ssd_chunk_scan_noalloc: ssd_chunk_scan with the library's static per-GPU scratch
+    instead of a workspace (no device allocation by the library; outputs and taps are still
+    allocated here unless passed in, e.g. y=).  Workspaces above 128 MiB are refused."""
+    if kw.get("workspace") is not None:
+        raise ValueError("ssd_chunk_scan_noalloc takes no workspace")
+    kw.pop("workspace", None)
+    return ssd_chunk_scan(*args, _noalloc=True, **kw)
 
 
 def ssd_chunk_scan_fp16(x: torch.Tensor, dt: torch.Tensor, A: torch.Tensor, B: torch.Tensor,
@@ -394,7 +416,8 @@ def ssd_chunk_scan_fp16(x: torch.Tensor, dt: torch.Tensor, A: torch.Tensor, B: t
     if final_state:
         out["final_state"] = torch.empty((Bt, H, P, N), dtype=torch.float32, device=dev)
         a.final_state = _ptr(out["final_state"])
-    a.workspace, a.workspace_bytes = _ptr(workspace), workspace.numel()
+    if workspace is not None:
+        a.workspace, a.workspace_bytes = _ptr(workspace), workspace.numel()
     if stage_events is not None:
         a.stage_events = ctypes.cast(stage_events, ctypes.c_void_p)
     st = lib().ssdi8_ssd_chunk_scan_fp16(ctypes.byref(d), ctypes.byref(a), _stream(stream))
@@ -470,7 +493,8 @@ def calibrate(x: torch.Tensor, dt: torch.Tensor, A: torch.Tensor, B: torch.Tenso
     a.B_scale, a.C_scale = _ptr(out["alpha_B"]), _ptr(out["alpha_C"])
     a.xs_scale, a.state_scale = _ptr(out["alpha_Xs"]), _ptr(out["alpha_S"])
     a.cb_scale, a.corr = _ptr(out["alpha_CB"]), _ptr(out["corr"])
-    a.workspace, a.workspace_bytes = _ptr(workspace), workspace.numel()
+    if workspace is not None:
+        a.workspace, a.workspace_bytes = _ptr(workspace), workspace.numel()
     st = lib().ssdi8_calibrate(ctypes.byref(d), ctypes.byref(a), _stream(stream))
     _check(st, "ssdi8_calibrate")
     return out
