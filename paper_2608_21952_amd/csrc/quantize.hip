@@ -164,48 +164,61 @@ __global__ __launch_bounds__(256) void absmax_granules(const T* __restrict__ src
 // that never straddle two granules (m % kE == 0): the rows are the outer loop and each thread
 // owns fixed units (columns) of them, so the granule of each of its values never changes and
 // its running maxima stay in registers (kE of them per column for CHANNEL, one otherwise).
-// A block is TR rows x TC columns of threads; LDS atomics only when a thread leaves a column.
+// A block is TR rows x TC columns of threads, one block per CU.  When a thread leaves a column,
+// the lanes of one granule first combine their maxima by shuffles (gsz consecutive lanes:
+// m / kE for GROUP, the whole wave for TENSOR, one lane for CHANNEL), so that one lane per
+// granule and wave updates LDS, and each block updates each global word once.
 template <typename T>
 __global__ __launch_bounds__(256) void absmax_cols(const T* __restrict__ src,
                                                    uint32_t* __restrict__ acc, int gran,
                                                    int64_t rows, int cols, int tc, int m,
-                                                   int ngran) {
+                                                   int ngran, int gsz) {
   constexpr int kE = 16 / sizeof(T);
   __shared__ uint32_t smax[kMaxGranules];
   for (int i = threadIdx.x; i < ngran; i += blockDim.x) smax[i] = 0u;
   __syncthreads();
   const int tx = threadIdx.x % tc, ty = threadIdx.x / tc, tr = blockDim.x / tc;
-  for (int col = tx; col < cols; col += tc) {
+  const int lane = threadIdx.x & 63;
+  for (int col0 = 0; col0 < cols; col0 += tc) {
+    const int col = col0 + tx;
+    const bool live = col < cols;
     float mx[kE];
 #pragma unroll
     for (int e = 0; e < kE; ++e) mx[e] = 0.0f;
-    for (int64_t row = (int64_t)blockIdx.x * tr + ty; row < rows; row += (int64_t)gridDim.x * tr) {
-      const uint4 u = reinterpret_cast<const uint4*>(src + (row * cols + col) * kE)[0];
-      if constexpr (sizeof(T) == 2) {
+    if (live) {
+#pragma unroll 4
+      for (int64_t row = (int64_t)blockIdx.x * tr + ty; row < rows;
+           row += (int64_t)gridDim.x * tr) {
+        const uint4 u = reinterpret_cast<const uint4*>(src + (row * cols + col) * kE)[0];
         const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+        if constexpr (sizeof(T) == 2) {
 #pragma unroll
-        for (int e = 0; e < kE; ++e) {
-          const float v = (float)__builtin_bit_cast(
-              _Float16, (uint16_t)((e & 1) ? (w[e >> 1] >> 16) : (w[e >> 1] & 0xffffu)));
-          mx[e] = __builtin_fmaxf(mx[e], __builtin_fabsf(v));
+          for (int e = 0; e < kE; ++e) {
+            const float v = (float)__builtin_bit_cast(
+                _Float16, (uint16_t)((e & 1) ? (w[e >> 1] >> 16) : (w[e >> 1] & 0xffffu)));
+            mx[e] = __builtin_fmaxf(mx[e], __builtin_fabsf(v));
+          }
+        } else {
+#pragma unroll
+          for (int e = 0; e < kE; ++e)
+            mx[e] = __builtin_fmaxf(mx[e], __builtin_fabsf(__uint_as_float(w[e])));
         }
-      } else {
-        const uint32_t w[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-        for (int e = 0; e < kE; ++e)
-          mx[e] = __builtin_fmaxf(mx[e], __builtin_fabsf(__uint_as_float(w[e])));
       }
     }
     if (gran == 2) {
+      if (live) {
 #pragma unroll
-      for (int e = 0; e < kE; ++e)
-        if (mx[e] > 0.0f) atomicMax(&smax[col * kE + e], __float_as_uint(mx[e]));
+        for (int e = 0; e < kE; ++e)
+          if (mx[e] > 0.0f) atomicMax(&smax[col * kE + e], __float_as_uint(mx[e]));
+      }
     } else {
       float v = mx[0];
 #pragma unroll
       for (int e = 1; e < kE; ++e) v = __builtin_fmaxf(v, mx[e]);
+      // lanes of one granule are gsz consecutive lanes starting at a multiple of gsz
+      for (int o = gsz >> 1; o > 0; o >>= 1) v = __builtin_fmaxf(v, __shfl_xor(v, o, 64));
       const int gi = gran == 0 ? 0 : (col * kE) / m;
-      if (v > 0.0f) atomicMax(&smax[gi], __float_as_uint(v));
+      if (live && (lane & (gsz - 1)) == 0 && v > 0.0f) atomicMax(&smax[gi], __float_as_uint(v));
     }
   }
   __syncthreads();
@@ -269,9 +282,15 @@ hipError_t quantize_impl(const T* src, int64_t b, int64_t l, int64_t k, int64_t 
       const int tc = cols < 64 ? (int)cols : 64;
       const int tr = 256 / tc;
       const int64_t rows = b * l;
-      hipLaunchKernelGGL(absmax_cols<T>, dim3((unsigned)grid_for(rows, tr, 2048)), dim3(256), 0,
+      // lanes sharing a granule: the wave (TENSOR, when a wave holds columns of one row only),
+      // the m / kE lanes of one group (GROUP, when that is a power of two dividing tc), else one
+      int gsz = 1;
+      const int upr = (int)(m / kE);   // units per granule row for GROUP
+      if (gran == 0 && tc == 64) gsz = 64;
+      if (gran == 1 && upr > 0 && (upr & (upr - 1)) == 0 && tc % upr == 0) gsz = upr;
+      hipLaunchKernelGGL(absmax_cols<T>, dim3((unsigned)grid_for(rows, tr, 256)), dim3(256), 0,
                          st, src, reinterpret_cast<uint32_t*>(scale), gran, rows, (int)cols, tc,
-                         (int)m, ngran);
+                         (int)m, ngran, gsz);
     } else if (n > 0) {
       hipLaunchKernelGGL(absmax_granules<T>, dim3((unsigned)grid_for(n, 256, 2048)), dim3(256),
                          0, st, src, reinterpret_cast<uint32_t*>(scale), gran, n, k, m, ngran);
