@@ -8,7 +8,10 @@
 // LDS as int8 [256][128] tiles whose 16-byte chunks are XOR-swizzled by row, so that the MFMA
 // operand reads (16 bytes per lane, 32 rows x 2 K-halves per wave) and the row writes are free
 // of bank conflicts.  Its tiles are spread over the 8 waves; each is 4 MFMAs over n with the
-// operands read straight from LDS in the per-lane K-slice layout of v_mfma_i32_32x32x32_i8.
+// operands read straight from LDS in the per-lane K-slice layout of v_mfma_i32_32x32x32_i8,
+// formed transposed (MFMA rows = source tokens i, columns = target tokens j) so that a lane holds
+// one target row: one requant multiplier per lane, and its CB-order 16-byte slice is complete
+// after one exchange of two dwords with the other half-wave.
 //
 // Outputs for the later kernels are written in MFMA fragment order (frag.hpp): a wave reads
 // each operand fragment as one contiguous 1 KB run.
@@ -100,7 +103,6 @@ __global__ __launch_bounds__(kThreads) void chunk_bmm_kernel(
     int* __restrict__ timeouts, int L, int G, int nc, int S) {
   __shared__ __attribute__((aligned(16))) int8_t s_c[kQ * kN];
   __shared__ __attribute__((aligned(16))) int8_t s_b[kQ * kN];
-  __shared__ __attribute__((aligned(16))) int8_t s_stage[kWaves * 1024];
   __shared__ float s_m[kQ];
 
   const int t = threadIdx.x, lane = t & 63;
@@ -190,7 +192,6 @@ __global__ __launch_bounds__(kThreads) void chunk_bmm_kernel(
 
   // ---- the causal 32x32 tiles of row blocks [jlo, jhi) (global tile numbers [jlo (jlo + 1) / 2,
   //      jhi (jhi + 1) / 2)), wave w taking the part's tiles w, w + 8, ...
-  int8_t* stage = s_stage + wv * 1024;
   const int hl = lane >> 5, lr = lane & 31;
   const int tile_end = jhi * (jhi + 1) / 2;
   for (int tile = jlo * (jlo + 1) / 2 + wv; tile < tile_end; tile += kWaves) {
@@ -206,14 +207,15 @@ __global__ __launch_bounds__(kThreads) void chunk_bmm_kernel(
       // the C_q rows of block jt, in ChunkScan1 fragment order
       int8_t* cdst = cq_frag + cg * (size_t)kQ * kN;
       if (cq_perm) {
-        // permuted kslice order: lane (j, h) takes n = 8 g + 4 h + i; it holds n = 16 h + [0, 16)
-        // and swaps the other half-wave's two runs of 4 with lane l ^ 32
+        // permuted kslice order: lane (j, h) holds n = 8 g + 4 h + [0, 4) at dword g; it has
+        // n = 16 h + [0, 16): the lower half-wave keeps its dwords 0 and 2 and takes the upper
+        // half's 0 and 2, the upper half keeps 1 and 3 and takes the lower half's 1 and 3
 #pragma unroll
         for (int ks = 0; ks < kN / 32; ++ks) {
-          const int s0 = hl ? a[ks][0] : a[ks][1], s1 = hl ? a[ks][2] : a[ks][3];
-          const int r0 = __shfl_xor(s0, 32, 64), r1 = __shfl_xor(s1, 32, 64);
-          const v4i o = hl ? v4i{r0, r1, a[ks][1], a[ks][3]} : v4i{a[ks][0], a[ks][2], r0, r1};
-          *reinterpret_cast<v4i*>(cdst + ((size_t)jt * (kN / 32) + ks) * 1024 + lane * 16) = o;
+          const auto s01 = __builtin_amdgcn_permlane32_swap(a[ks][0], a[ks][1], false, false);
+          const auto s23 = __builtin_amdgcn_permlane32_swap(a[ks][2], a[ks][3], false, false);
+          *reinterpret_cast<uint4*>(cdst + ((size_t)jt * (kN / 32) + ks) * 1024 + lane * 16) =
+              make_uint4(s01[0], s23[0], s01[1], s23[1]);
         }
       } else {
 #pragma unroll
@@ -222,40 +224,44 @@ __global__ __launch_bounds__(kThreads) void chunk_bmm_kernel(
                                                              kN)) = a[ks];
       }
     }
+    // CB32^T: lane l holds target row j = 32 jt + l % 32 and, in register r, source token
+    // i = 32 it + 8 (r / 4) + 4 (l / 32) + r % 4, so one requant multiplier serves the lane
     v16i acc = {};
 #pragma unroll
     for (int ks = 0; ks < kN / 32; ++ks)
-      acc = __builtin_amdgcn_mfma_i32_32x32x32_i8(a[ks], bb[ks], acc, 0, 0, 0);
-    // requantize into this wave's 1 KB stage in CB fragment order, then one 16-byte store per
-    // lane (the stage is private to the wave, whose LDS accesses complete in order)
-    const size_t obase = cg * (size_t)kQ * kQ;
-    const int i = it * 32 + lr;
-    int v[16], q[16];
+      acc = __builtin_amdgcn_mfma_i32_32x32x32_i8(bb[ks], a[ks], acc, 0, 0, 0);
+    const int j = jt * 32 + lr;
+    const float m = s_m[j];
+    uint32_t d[4];   // codes + 128 of i = 32 it + 8 g4 + 4 (l / 32) + [0, 4)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int jj = 8 * (r >> 2) + 4 * hl + (r & 3);
-      const bool keep = i <= jt * 32 + jj;
-      v[r] = keep ? acc[r] : 0;
-      q[r] = keep ? requant_i8(v[r], s_m[jt * 32 + jj]) : 0;
-      stage[frag::cb_inblock(jj, lr)] = (int8_t)(q[r] ^ 0x80);   // stored as q + 128
+    for (int g4 = 0; g4 < 4; ++g4) {
+      uint32_t bits[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int ii = 8 * g4 + 4 * hl + e;
+        const bool keep = it < jt || ii <= lr;
+        bits[e] = keep ? requant_bits(acc[4 * g4 + e], m) : 0x4B400000u;   // 0x4B400000: code 0
+      }
+      d[g4] = pack_lo4(bits[0], bits[1], bits[2], bits[3]) ^ 0x80808080u;   // stored as q + 128
     }
     if (cbq_tap || cb32_tap) {   // row-major debug copies
+      const size_t orow = cg * (size_t)kQ * kQ + (size_t)j * kQ + it * 32;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const size_t o = obase + (size_t)(jt * 32 + 8 * (r >> 2) + 4 * hl + (r & 3)) * kQ + i;
-        if (cbq_tap) cbq_tap[o] = (int8_t)q[r];
-        if (cb32_tap) cb32_tap[o] = v[r];
+        const int ii = 8 * (r >> 2) + 4 * hl + (r & 3);
+        const bool keep = it < jt || ii <= lr;
+        if (cbq_tap) cbq_tap[orow + ii] = (int8_t)(((d[r >> 2] >> (8 * (r & 3))) & 0xffu) ^ 0x80u);
+        if (cb32_tap) cb32_tap[orow + ii] = keep ? acc[r] : 0;
       }
     }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    const uint4 o = *reinterpret_cast<const uint4*>(stage + lane * 16);
+    // CB order wants i = 32 it + 8 (l / 32) + [0, 8) and 16 + that: the lower half-wave keeps
+    // runs 0 and 2 and takes the upper half's runs 0 and 2, the upper half keeps runs 1 and 3
+    // and takes the lower half's runs 1 and 3 (lanes l and l ^ 32 exchange one dword each)
+    const auto s01 = __builtin_amdgcn_permlane32_swap(d[0], d[1], false, false);
+    const auto s23 = __builtin_amdgcn_permlane32_swap(d[2], d[3], false, false);
     *reinterpret_cast<uint4*>(cbq_frag + cg * (size_t)frag::kCbChunkBytes +
-                              (size_t)frag::cb_block(jt, it) * 1024 + lane * 16) = o;
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+                              (size_t)frag::cb_block(jt, it) * 1024 + lane * 16) =
+        make_uint4(s01[0], s01[1], s23[0], s23[1]);
   }
 }
 
