@@ -41,7 +41,7 @@ __device__ __forceinline__ double lut_of_chunk(const float* dt, const float* A, 
   float dtv = dt[(tok0 + t) * H + h];
   if (dt_softplus) dtv = softplus_f32(dtv);
   const float dA = dtv * A[h];
-  const double cs = block_scan_f64_256((double)dA, s_scan);
+  const double cs = block_scan_f64_256(dA, s_scan, s_lut);
   if (t == kQ - 1) *s_last = cs;
   __syncthreads();
   const double last = *s_last;
@@ -59,7 +59,7 @@ __global__ __launch_bounds__(256) void calib_xs_kernel(const XT* __restrict__ x,
                                                        uint32_t* __restrict__ xs_amax, int L,
                                                        int H, int nc) {
   __shared__ float s_lut[kQ];
-  __shared__ double s_scan[4];
+  __shared__ double s_scan[kScanScratch];
   __shared__ double s_last;
   __shared__ float s_m[8][kP];
   const int t = threadIdx.x;
@@ -98,7 +98,7 @@ __global__ __launch_bounds__(256) void calib_state_kernel(
     double* __restrict__ dec64, int L, int H, int G, int nc) {
   __shared__ __attribute__((aligned(16))) uint8_t s_x[kP * kXS];
   __shared__ float s_lut[kQ];
-  __shared__ double s_scan[4];
+  __shared__ double s_scan[kScanScratch];
   __shared__ double s_last;
   const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
   const int w = blockIdx.x;

@@ -93,7 +93,7 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
     float aS[kP];
     float cr[kP];
     double r[8];         // r_t: cs at the last token of block t
-    double scan[4];
+    double scan[kScanScratch];
     int misc[4];         // single pass: ticket, q_d, look-back anchor
     int lq[kLook];       // single pass: Q(Decay) of chunks c-1, c-2, ... (flag words' low half)
     // x^T [p][i] fp16: the ChunkScan2 MFMA operand and, for fp16 x, the D skip operand; then
@@ -183,7 +183,7 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
   //      the whole layer (and X_scaled of the single pass needs exactly that value)
   if (dt_softplus) dtv = softplus_f32(dtv);
   const float dA = dtv * A[h];
-  const double cs = block_scan_f64_256((double)dA, s_scan);
+  const double cs = block_scan_f64_256(dA, s_scan, sm.lut);
   if ((t & 31) == 31) s_r[t >> 5] = cs;
   if (t < kP) {
     s_aS[t] = aSv;

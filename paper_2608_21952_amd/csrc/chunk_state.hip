@@ -63,7 +63,7 @@ __global__ __launch_bounds__(256, sizeof(XT) == 2 ? 6 : 4) void chunk_state_kern
   __shared__ float s_lut[kQ];
   __shared__ float s_inv[kP];
   __shared__ float s_ms[kP];
-  __shared__ double s_scan[4];
+  __shared__ double s_scan[kScanScratch];
   __shared__ double s_last;
 
   const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
@@ -91,7 +91,7 @@ __global__ __launch_bounds__(256, sizeof(XT) == 2 ? 6 : 4) void chunk_state_kern
   if (dt_softplus) dtv = softplus_f32(dtv);
   if (dt_tap) dt_tap[(tok0 + t) * H + h] = dtv;
   const float dA = dtv * A[h];
-  const double cs = block_scan_f64_256((double)dA, s_scan);
+  const double cs = block_scan_f64_256<true>(dA, s_scan, s_lut);
   if (t == kQ - 1) s_last = cs;
   if (t < kP) {
     const float axs = xs_per_head ? xs_scale[h] : xs_scale[h * kP + t];

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "exact_sum.hpp"
+
 namespace ssdi8 {
 
 // Fixed problem geometry of the kernels: headdim P, state size N, chunk length Q.
@@ -201,26 +203,82 @@ __device__ __forceinline__ double dpp_add_f64(double v) {
   return v + __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
 }
 
-// Inclusive prefix sum over the 256 threads of a block in fp64.  The in-chunk sums of fp32
-// decay increments are exact in fp64 (the terms of one chunk span few binades), so the tree
-// order used here gives the same values as a sequential sum.  Within a wave: shifts by 1, 2, 4,
-// 8 lanes inside each row of 16 (row_shr), then the last lane of row 0 / 2 into rows 1 / 3
-// (row_bcast:15) and the last lane of row 1 into rows 2 and 3 (row_bcast:31), all in registers;
-// across the four waves through `scratch` (4 doubles).
-__device__ __forceinline__ double block_scan_f64_256(double v, double* scratch) {
+// Packed exponent range of a term for the exactness test of block_scan_f64_256: low half
+// e + 256, high half 256 - e, with e the exponent of |v| in [2^(e-1), 2^e); subnormals take
+// e = -149 (a lower bound, which only makes the test stricter); zero gives 0, the identity of the
+// halfwise max.
+__device__ __forceinline__ uint32_t exp_range_f32(float v) {
+  const uint32_t b = __float_as_uint(v) & 0x7fffffffu;
+  if (b == 0) return 0u;
+  const int f = (int)(b >> 23);
+  const int e = f ? f - 126 : -149;
+  return (uint32_t)(e + 256) | ((uint32_t)(256 - e) << 16);
+}
+typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t max_u16x2(uint32_t a, uint32_t b) {
+  return __builtin_bit_cast(uint32_t, __builtin_elementwise_max(__builtin_bit_cast(u16x2, a),
+                                                                __builtin_bit_cast(u16x2, b)));
+}
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ uint32_t dpp_max_u16x2(uint32_t v) {
+  return max_u16x2(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, kCtrl, kRowMask, 0xf,
+                                                            false));
+}
+
+// Inclusive prefix sum over the 256 threads of a block of fp32 terms, exact and rounded once to
+// fp64.  A tree of fp64 additions gives it when every partial sum is exact: the nonzero terms are
+// multiples of 2^(e_min - 24) and every partial sum stays below 2^(e_max + 8), so it holds when
+// e_max - e_min <= 21 (e: the exponent of |v| in [2^(e-1), 2^e)).  That is the case the block
+// tests for; the tree then runs within a wave as shifts by 1, 2, 4, 8 lanes inside each row of
+// 16 (row_shr), the last lane of row 0 / 2 into rows 1 / 3 (row_bcast:15) and the last lane of
+// row 1 into rows 2 and 3 (row_bcast:31), all in registers, and across the four waves through
+// `scratch`.  A block with a wider range (only inputs far outside the method's domain, e.g. dt
+// over 20 binades within one chunk) instead sums each prefix exactly (exact_sum_f32) from `stage`.
+// scratch: kScanScratch doubles; stage: 256 floats of LDS that the caller writes only after this
+// returns.  Every thread of the block must call it.
+// kOutlined: the exact path as a call (for kernels whose registers are tight where they scan; the
+// call keeps the rare path's registers out of the rest of the kernel).
+constexpr int kScanScratch = 6;
+static __device__ __noinline__ double exact_sum_f32_outlined(const float* v, int n) {
+  return exact_sum_f32(v, n);
+}
+template <bool kOutlined = false>
+__device__ __forceinline__ double block_scan_f64_256(float term, double* scratch, float* stage) {
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
+  double v = (double)term;
+  uint32_t er = exp_range_f32(term);
   v = dpp_add_f64<0x111, 0xf>(v);
   v = dpp_add_f64<0x112, 0xf>(v);
   v = dpp_add_f64<0x114, 0xf>(v);
   v = dpp_add_f64<0x118, 0xf>(v);
   v = dpp_add_f64<0x142, 0xa>(v);
   v = dpp_add_f64<0x143, 0xc>(v);
-  if (lane == 63) scratch[w] = v;
+  er = dpp_max_u16x2<0x111, 0xf>(er);
+  er = dpp_max_u16x2<0x112, 0xf>(er);
+  er = dpp_max_u16x2<0x114, 0xf>(er);
+  er = dpp_max_u16x2<0x118, 0xf>(er);
+  er = dpp_max_u16x2<0x142, 0xa>(er);
+  er = dpp_max_u16x2<0x143, 0xc>(er);
+  uint32_t* sr = reinterpret_cast<uint32_t*>(scratch + 4);
+  if (lane == 63) {
+    scratch[w] = v;
+    sr[w] = er;
+  }
   __syncthreads();
-  double pre = 0.0;
-  for (int i = 0; i < w; ++i) pre += scratch[i];
-  return v + pre;
+  const uint32_t r = max_u16x2(max_u16x2(sr[0], sr[1]), max_u16x2(sr[2], sr[3]));
+  const int e_max = (int)(r & 0xffffu) - 256, e_min = 256 - (int)(r >> 16);
+  if (r == 0u || e_max - e_min <= 21) {
+    double pre = 0.0;
+    for (int i = 0; i < w; ++i) pre += scratch[i];
+    return v + pre;
+  }
+  stage[threadIdx.x] = term;
+  __syncthreads();
+  const double cs = kOutlined ? exact_sum_f32_outlined(stage, threadIdx.x + 1)
+                              : exact_sum_f32(stage, threadIdx.x + 1);
+  __syncthreads();
+  return cs;
 }
 
 // Pack the low bytes of four ints into one dword (byte i = v_i).

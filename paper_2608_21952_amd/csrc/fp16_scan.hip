@@ -69,7 +69,7 @@ __global__ __launch_bounds__(256, 3) void fp16_scan_kernel(
     float csr[kQ];       // cs_i - r_{I-1}
     float R[8][8];       // exp(r_a - r_b), b <= a
     double r[8];
-    double scan[4];
+    double scan[kScanScratch];
     uint8_t xT[kP * kXTS];
   };
   __shared__ Smem sm;
@@ -103,7 +103,7 @@ __global__ __launch_bounds__(256, 3) void fp16_scan_kernel(
   float dtv = dt[(tok0 + t) * H + h];
   if (dt_softplus) dtv = softplus_f32(dtv);   // the dt of this layer's ChunkState
   const float dA = dtv * A[h];
-  const double cs = block_scan_f64_256((double)dA, sm.scan);
+  const double cs = block_scan_f64_256(dA, sm.scan, sm.u);
   if ((t & 31) == 31) s_r[t >> 5] = cs;
   __syncthreads();
   {

@@ -48,7 +48,7 @@ __global__ __launch_bounds__(256) void fp16_state_kernel(
     float* __restrict__ dec, int L, int H, int G, int nc) {
   __shared__ __attribute__((aligned(16))) uint8_t s_x[kP * kXS];
   __shared__ float s_lut[kQ];
-  __shared__ double s_scan[4];
+  __shared__ double s_scan[kScanScratch];
   __shared__ double s_last;
 
   const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
@@ -72,7 +72,7 @@ __global__ __launch_bounds__(256) void fp16_state_kernel(
   float dtv = dt[(tok0 + t) * H + h];
   if (dt_softplus) dtv = softplus_f32(dtv);
   const float dA = dtv * A[h];
-  const double cs = block_scan_f64_256((double)dA, s_scan);
+  const double cs = block_scan_f64_256(dA, s_scan, s_lut);
   if (t == kQ - 1) s_last = cs;
   __syncthreads();
   const double last = s_last;
