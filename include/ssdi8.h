@@ -76,8 +76,9 @@ typedef struct {
  *            compute_scale = 1: written with fl32(absmax / 127) of each granule (1 for an
  *            all-zero granule), then used.  Dynamic TENSOR/GROUP/CHANNEL modes support at most
  *            8192 granules (SSDI8_ERR_UNSUPPORTED beyond); TOKEN mode any number.
- *   dst      device int8 [b, l, k, m], 16-byte aligned:
- *            dst = clamp(rne(fl32(src * fl32(1 / scale))), -127, 127).
+ *   dst      device int8 [b, l, k, m], 16-byte aligned, not overlapping src:
+ *            dst = clamp(rne(fl32(src * fl32(1 / scale))), -127, 127).  With compute_scale = 1
+ *            it also holds partial maxima while the steps are computed, before the codes.
  *   b*l == 0 is valid: src and dst may then be NULL; nothing is quantized (dynamic
  *   TENSOR/GROUP/CHANNEL steps are set to 1, TOKEN has no steps).
  * Errors: NULL scale, NULL src/dst with b*l > 0, negative b/l, k or m < 1, bad dtype/gran,

@@ -164,13 +164,16 @@ __global__ __launch_bounds__(256) void absmax_granules(const T* __restrict__ src
 // that never straddle two granules (m % kE == 0): the rows are the outer loop and each thread
 // owns fixed units (columns) of them, so the granule of each of its values never changes and
 // its running maxima stay in registers (kE of them per column for CHANNEL, one otherwise).
-// A block is TR rows x TC columns of threads, one block per CU.  When a thread leaves a column,
-// the lanes of one granule first combine their maxima by shuffles (gsz consecutive lanes:
-// m / kE for GROUP, the whole wave for TENSOR, one lane for CHANNEL), so that one lane per
-// granule and wave updates LDS, and each block updates each global word once.
+// A block is TR rows x TC columns of threads.  When a thread leaves a column, the lanes of one
+// granule first combine their maxima by shuffles (gsz consecutive lanes: m / kE for GROUP, the
+// whole wave for TENSOR, one lane for CHANNEL), so that one lane per granule and wave updates
+// LDS.  Each block then writes its ngran maxima to part[block] (all of them, zeros included),
+// which absmax_partials_to_step reduces; or, with part NULL, updates each global word of `acc`
+// once by atomic max.
 template <typename T>
 __global__ __launch_bounds__(256) void absmax_cols(const T* __restrict__ src,
-                                                   uint32_t* __restrict__ acc, int gran,
+                                                   uint32_t* __restrict__ acc,
+                                                   uint32_t* __restrict__ part, int gran,
                                                    int64_t rows, int cols, int tc, int m,
                                                    int ngran, int gsz) {
   constexpr int kE = 16 / sizeof(T);
@@ -222,8 +225,39 @@ __global__ __launch_bounds__(256) void absmax_cols(const T* __restrict__ src,
     }
   }
   __syncthreads();
-  for (int i = threadIdx.x; i < ngran; i += blockDim.x)
-    if (smax[i]) atomicMax(&acc[i], smax[i]);
+  if (part) {
+    for (int i = threadIdx.x; i < ngran; i += blockDim.x)
+      part[(size_t)blockIdx.x * ngran + i] = smax[i];
+  } else {
+    for (int i = threadIdx.x; i < ngran; i += blockDim.x)
+      if (smax[i]) atomicMax(&acc[i], smax[i]);
+  }
+}
+
+// step[g] = max over blocks of part[block][g] (float bits) / 127, or 1 for an all-zero granule
+// (as absmax_to_step): one block per granule.
+__global__ __launch_bounds__(256) void absmax_partials_to_step(const uint32_t* __restrict__ part,
+                                                               int nblocks, int ngran,
+                                                               float* __restrict__ scale) {
+  __shared__ uint32_t wmax[4];
+  const int g = blockIdx.x;
+  uint32_t v = 0u;
+  for (int b = threadIdx.x; b < nblocks; b += blockDim.x) {
+    const uint32_t x = part[(size_t)b * ngran + g];
+    v = x > v ? x : v;
+  }
+  for (int o = 32; o > 0; o >>= 1) {
+    const uint32_t x = (uint32_t)__shfl_xor((int)v, o, 64);
+    v = x > v ? x : v;
+  }
+  if ((threadIdx.x & 63) == 0) wmax[threadIdx.x >> 6] = v;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int w = 1; w < 4; ++w) v = wmax[w] > v ? wmax[w] : v;
+    v = wmax[0] > v ? wmax[0] : v;
+    const float a = __uint_as_float(v) / 127.0f;
+    scale[g] = (a == 0.0f) ? 1.0f : a;
+  }
 }
 
 __global__ void absmax_to_step(float* scale, int n) {
@@ -255,6 +289,10 @@ __global__ __launch_bounds__(256) void quant_token_dynamic(const T* __restrict__
   for (int64_t i = lane; i < m; i += 64) dst[row * m + i] = (int8_t)quant_i8((float)s[i], inv);
 }
 
+// blocks of the dynamic absmax (several per CU for loads in flight; their partial maxima are
+// reduced by a second kernel, so more blocks cost no atomics)
+constexpr int64_t kAbsmaxBlocks = 512;
+
 inline int64_t grid_for(int64_t items, int per_block = 256, int64_t cap = 65536) {
   int64_t g = (items + per_block - 1) / per_block;
   return g < 1 ? 1 : (g > cap ? cap : g);
@@ -273,8 +311,6 @@ hipError_t quantize_impl(const T* src, int64_t b, int64_t l, int64_t k, int64_t 
   }
   if (compute_scale) {
     const int ngran = gran == 0 ? 1 : (gran == 1 ? (int)k : (int)(k * m));
-    hipLaunchKernelGGL(fill_u32, dim3((unsigned)grid_for(ngran)), dim3(256), 0, st,
-                       reinterpret_cast<uint32_t*>(scale), (int64_t)ngran, 0u);
     constexpr int kE = 16 / sizeof(T);
     const int64_t cols = k * m / kE;
     if (n > 0 && m % kE == 0 && cols <= ((int64_t)1 << 20)) {
@@ -288,15 +324,35 @@ hipError_t quantize_impl(const T* src, int64_t b, int64_t l, int64_t k, int64_t 
       const int upr = (int)(m / kE);   // units per granule row for GROUP
       if (gran == 0 && tc == 64) gsz = 64;
       if (gran == 1 && upr > 0 && (upr & (upr - 1)) == 0 && tc % upr == 0) gsz = upr;
-      hipLaunchKernelGGL(absmax_cols<T>, dim3((unsigned)grid_for(rows, tr, 256)), dim3(256), 0,
-                         st, src, reinterpret_cast<uint32_t*>(scale), gran, rows, (int)cols, tc,
-                         (int)m, ngran, gsz);
-    } else if (n > 0) {
-      hipLaunchKernelGGL(absmax_granules<T>, dim3((unsigned)grid_for(n, 256, 2048)), dim3(256),
-                         0, st, src, reinterpret_cast<uint32_t*>(scale), gran, n, k, m, ngran);
+      // the blocks' partial maxima go to dst, which holds nothing yet (it is written by the
+      // quantization that follows), when they fit there; else one atomic max per block
+      int64_t nb = grid_for(rows, tr, kAbsmaxBlocks);
+      const int64_t room = n / (4 * (int64_t)ngran);
+      if (room >= 1) {
+        if (nb > room) nb = room;
+        uint32_t* part = reinterpret_cast<uint32_t*>(dst);
+        hipLaunchKernelGGL(absmax_cols<T>, dim3((unsigned)nb), dim3(256), 0, st, src, nullptr,
+                           part, gran, rows, (int)cols, tc, (int)m, ngran, gsz);
+        hipLaunchKernelGGL(absmax_partials_to_step, dim3((unsigned)ngran), dim3(256), 0, st,
+                           part, (int)nb, ngran, scale);
+      } else {
+        hipLaunchKernelGGL(fill_u32, dim3((unsigned)grid_for(ngran)), dim3(256), 0, st,
+                           reinterpret_cast<uint32_t*>(scale), (int64_t)ngran, 0u);
+        hipLaunchKernelGGL(absmax_cols<T>, dim3((unsigned)grid_for(rows, tr, 256)), dim3(256), 0,
+                           st, src, reinterpret_cast<uint32_t*>(scale), nullptr, gran, rows,
+                           (int)cols, tc, (int)m, ngran, gsz);
+        hipLaunchKernelGGL(absmax_to_step, dim3((unsigned)((ngran + 255) / 256)), dim3(256), 0,
+                           st, scale, ngran);
+      }
+    } else {
+      hipLaunchKernelGGL(fill_u32, dim3((unsigned)grid_for(ngran)), dim3(256), 0, st,
+                         reinterpret_cast<uint32_t*>(scale), (int64_t)ngran, 0u);
+      if (n > 0)
+        hipLaunchKernelGGL(absmax_granules<T>, dim3((unsigned)grid_for(n, 256, 2048)), dim3(256),
+                           0, st, src, reinterpret_cast<uint32_t*>(scale), gran, n, k, m, ngran);
+      hipLaunchKernelGGL(absmax_to_step, dim3((unsigned)((ngran + 255) / 256)), dim3(256), 0, st,
+                         scale, ngran);
     }
-    hipLaunchKernelGGL(absmax_to_step, dim3((unsigned)((ngran + 255) / 256)), dim3(256), 0, st,
-                       scale, ngran);
   }
   if (n == 0) return hipGetLastError();
   if (sizeof(T) == 2 && m % 8 == 0 && n < ((int64_t)1 << 31)) {

@@ -50,6 +50,24 @@ def test_quantize_dynamic_and_static(torch, ssdi8, dtype, gran):
     assert np.array_equal(q2.cpu().numpy(), q_ref)
 
 
+@pytest.mark.parametrize("shape", [(1, 1, 4, 128), (1, 3, 64, 16), (2, 4096, 8, 128)])
+@pytest.mark.parametrize("gran", ["tensor", "group", "channel"])
+def test_quantize_dynamic_steps_any_block_count(torch, ssdi8, shape, gran):
+    """The dynamic steps reduce per-block maxima kept in the output buffer while they fit there
+    (up to one block per 4 rows, many blocks at full size) and fall back to atomic maxima when
+    they do not (a single row with per-channel steps)."""
+    say(f"quantize_act dynamic shape={shape} gran={gran}")
+    rng = np.random.default_rng(3)
+    src = rng.standard_normal(shape) * np.exp(rng.uniform(-4, 4, (1, 1, shape[2], 1)))
+    src.reshape(-1)[rng.integers(0, src.size, 5)] *= 50
+    src = src.astype(np.float16)
+    q_ref, a_ref = oq.quantize_act(src, gran)
+    q, a = ssdi8.quantize_act(dev(src, torch), gran)
+    torch.cuda.synchronize()
+    assert np.array_equal(a.cpu().numpy().reshape(np.shape(a_ref)), a_ref)
+    assert np.array_equal(q.cpu().numpy(), q_ref)
+
+
 @pytest.mark.parametrize("m", [128, 24, 7])
 def test_quantize_odd_row_lengths(torch, ssdi8, m):
     say(f"quantize_act m={m}")
