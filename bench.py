@@ -29,7 +29,7 @@ MODULES = ("chunk_bmm", "chunk_state", "state_pass", "chunk_scan")
 SINGLE = ("chunk_bmm", "single_pass")
 SOURCE = {"single_pass": "chunk_scan"}      # kernel -> source file of its HIP code
 # headers every kernel source compiles in: a change to them is a change to the kernel
-KERNEL_HEADERS = ("common.hpp", "frag.hpp", "launch.hpp")
+KERNEL_HEADERS = ("common.hpp", "exact_sum.hpp", "frag.hpp", "launch.hpp")
 
 
 def kernel_source_sha256(kernel: str):
