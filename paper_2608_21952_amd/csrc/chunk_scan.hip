@@ -158,7 +158,9 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
     c = bc % nc;
     b = bc / nc;
   }
-  const int g = h / (H / G);
+  // wave-uniform (the division is done on the vector unit), so that the per-group steps are
+  // scalar loads and none of them drains the vector loads in flight
+  const int g = __builtin_amdgcn_readfirstlane(h / (H / G));
   const size_t tok0 = (size_t)b * L + (size_t)c * kQ;
   const size_t HP = (size_t)H * kP;
   const float aCB = cb_scale[g];
@@ -171,6 +173,21 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
   const float crv = (t < kP && corr) ? corr[h * kP + t] : 0.0f;
   // x tile (thread: channel pair (p0, p0+1), tokens [32 jb, 32 jb + 32))
   const int pp = t & 31, jb = t >> 5, p0 = 2 * pp;
+  // single pass: wave -> channel tile mt and state tiles ntb, ntb + 1; lane -> channel prow
+  const int hf = lane >> 5, mt = wv & 1, ntb = (wv >> 1) * 2;
+  const int prow = mt * 32 + (lane & 31);
+  // single pass: the X_q steps of this thread's channel pair, and the step of X_q and of S_q
+  // of this lane's channel for the ChunkState requant, requested with dt (unconditional loads,
+  // so that none of the waits before them is a full drain)
+  float ax0 = 1.0f, ax1 = 1.0f, axs = 1.0f, asp = 1.0f, abq = 1.0f;
+  if constexpr (kFused) {
+    const int xo = fs.xs_per_head ? 0 : 1;
+    ax0 = fs.xs_scale[xo * (h * kP + p0) + (1 - xo) * h];
+    ax1 = fs.xs_scale[xo * (h * kP + p0 + 1) + (1 - xo) * h];
+    axs = fs.xs_scale[xo * (h * kP + prow) + (1 - xo) * h];
+    asp = state_scale[h * kP + prow];
+    abq = fs.B_scale[g];
+  }
   typename Pair<XT>::raw xr[32];
   {
     const __amdgpu_buffer_rsrc_t xrs = buffer_rsrc(x + tok0 * HP + (size_t)h * kP);
@@ -238,8 +255,6 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
     // single pass: X_q^T [p][j] (int8, Eq. 7) first, in the bytes x^T takes later: each x
     // element is quantized once, by the thread that loaded it, with ChunkState's arithmetic
     __syncthreads();   // LUT_state complete
-    const float ax0 = fs.xs_per_head ? fs.xs_scale[h] : fs.xs_scale[h * kP + p0];
-    const float ax1 = fs.xs_per_head ? ax0 : fs.xs_scale[h * kP + p0 + 1];
     const float inv0 = 1.0f / ax0, inv1 = 1.0f / ax1;
     uint32_t w0[8], w1[8];
 #pragma unroll
@@ -263,17 +278,12 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
   }
   __syncthreads();
 
-  // single pass: wave -> channel tile mt and state tiles ntb, ntb + 1; lane -> channel prow
-  const int hf = lane >> 5, mt = wv & 1, ntb = (wv >> 1) * 2;
-  const int prow = mt * 32 + (lane & 31);
   uint32_t sq[2][4];   // S_q of the two tiles, byte r of word r / 4 = MFMA result row r
   if constexpr (kFused) {
     // ---- ChunkState (Eq. 7-8), transposed: S32^T = B_q^T X_q with the X_q^T fragments staged
     //      above.  Lane -> channel p = 32 mt + l % 32 and, per tile, the 16 state rows n of the
     //      permuted kslice order (frag.hpp), which is where the MFMA leaves them.
-    const float axs = fs.xs_per_head ? fs.xs_scale[h] : fs.xs_scale[h * kP + prow];
-    const float msp =
-        (float)(((double)axs * (double)fs.B_scale[g]) / (double)state_scale[h * kP + prow]);
+    const float msp = (float)(((double)axs * (double)abq) / (double)asp);
     {
       const __amdgpu_buffer_rsrc_t brs =
           buffer_rsrc(fs.bqT + (((size_t)b * nc + c) * G + g) * (size_t)kN * kQ);
@@ -514,11 +524,13 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
   uint2 y_first[8], y_second[8];
 
   // One j-block of 32 tokens: Scan1, Scan2 and the epilogue; fp16 output packed into yo.
-  auto jblock = [&](const int jt, uint2 (&yo)[8]) {
+  auto jblock = [&](int jt, uint2 (&yo)[8]) {
     // keeps the per-channel epilogue tables of the two calls from being loaded once and held
-    // across both (64 registers)
-    asm volatile("" ::: "memory");
+    // across both (64 registers), and their addresses from being computed ahead of the call
+    asm volatile("" : "+s"(jt) :: "memory");
     const int jrow = jt * 32 + pc;
+    // the C step of this row, for the epilogue (requested first: its wait then drains nothing)
+    const float ac = c_per_token ? C_scale[(tok0 + jrow) * G + g] : C_scale[g];
     const float csrj = s_csr[jrow];
     const float ej = __expf(csrj);                         // exp(cs_j - r_{J-1}), in (0, 1]
     const size_t orow = (tok0 + jrow) * HP + (size_t)h * kP;
@@ -682,7 +694,6 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
     }
     // -- epilogue of token row jrow: y = Y1 a_C exp(cs_j) a_S[p] + (y_diag + D x + corr[p])
     // a_C(j) exp(cs_j) = a_C(j) exp(cs_j - r_{J-1}) exp(r_{J-1})
-    const float ac = c_per_token ? C_scale[(tok0 + jrow) * G + g] : C_scale[g];
     const float eo = ac * ej * (jt ? __expf((float)s_r[jt - 1]) : 1.0f);
 #pragma unroll
     for (int pt = 0; pt < 2; ++pt) {
