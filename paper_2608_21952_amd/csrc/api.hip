@@ -40,6 +40,22 @@ hipError_t scratch_address(void** out) {
   return *out ? hipSuccess : hipErrorInvalidSymbol;
 }
 
+// Compute units of the current device, looked up once per device (0 if unknown).
+std::once_flag g_cus_once[kMaxDevices];
+int g_cus[kMaxDevices];
+
+int device_cus() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 0;
+  std::call_once(g_cus_once[dev], [dev]() {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+      n = 0;
+    g_cus[dev] = n;
+  });
+  return g_cus[dev];
+}
+
 using ssdi8::LayerDims;
 
 constexpr int64_t kMaxDim = (int64_t)1 << 31;
@@ -337,6 +353,10 @@ ssdi8_status ssdi8_ssd_chunk_scan(const ssdi8_dims* d, const ssdi8_scan_args* a,
     fs.nbh = ld.batch * ld.nheads;
     fs.nclass = ssdi8::sync_classes(fs.nbh);
     fs.spin_limit = 1 << 16;   // polls of ~1 us: a wait gives up after ~65 ms
+    // at most two rounds of workgroups (four per CU): the first loads of every item wait in
+    // full, so they are requested with the ticket for the item dispatch order predicts
+    const int64_t nitems = (int64_t)ld.batch * ld.nchunks * ld.nheads;
+    fs.speculate = nitems <= (int64_t)8 * device_cus() ? 1 : 0;
     e = ssdi8::launch_chunk_scan_fused(ld, static_cast<const _Float16*>(a->x), a->dt,
                                        a->dt_softplus, a->A, cq, a->C_scale, a->c_per_token, pin,
                                        cbq, a->cb_scale, a->state_scale, a->D, a->corr, a->y,

@@ -67,7 +67,9 @@ template <> struct Pair<float> {
   }
 };
 
-template <typename XT, typename YT, bool kFused>
+// kMode: 0 the separate ChunkScan, 1 the single pass, 2 the single pass with speculative first
+// loads (kSpec below).
+template <typename XT, typename YT, int kMode>
 __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
     const XT* __restrict__ x, const float* __restrict__ dt, const float* __restrict__ A,
     const int8_t* __restrict__ cq_frag, const float* __restrict__ C_scale, int c_per_token,
@@ -76,6 +78,8 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
     const float* __restrict__ Dv, const float* __restrict__ corr, int dt_softplus,
     YT* __restrict__ y, int32_t* __restrict__ y1_tap, int L, int H, int G, int nc,
     FusedState fs) {
+  constexpr bool kFused = kMode != 0;
+  constexpr bool kSpec = kMode == 2;
   // One LDS block with the small per-token tables first, so that their offsets fit the 16-bit
   // ds offset field (separate __shared__ arrays may be placed large-first).
   struct __attribute__((aligned(16))) Smem {
@@ -114,6 +118,32 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
   const int t = threadIdx.x, lane = t & 63;
   const int wv = __builtin_amdgcn_readfirstlane(t >> 6);   // wave-uniform, so block loops are scalar
   int b, c, h;
+  // x tile (thread: channel pair (p0, p0+1), tokens [32 jb, 32 jb + 32))
+  const int pp = t & 31, jb = t >> 5, p0 = 2 * pp;
+  // single pass: wave -> channel tile mt and state tiles ntb, ntb + 1; lane -> channel prow
+  const int hf = lane >> 5, mt = wv & 1, ntb = (wv >> 1) * 2;
+  const int prow = mt * 32 + (lane & 31);
+  // ---- loads in the order they are needed (vector loads complete in issue order): dt and the
+  //      per-channel tables first, so that the block scan and the tables wait for them alone
+  //      while the x tile is still in flight.  The single pass also requests the X_q steps of
+  //      this thread's channel pair and the steps of this lane's channel for the ChunkState
+  //      requant (unconditional loads, so that none of the waits before them is a full drain).
+  float dtv, aSv, crv, ax0 = 1.0f, ax1 = 1.0f, axs = 1.0f, asp = 1.0f, abq = 1.0f;
+  auto item_loads = [&](int bb, int cc, int hh) {
+    const int gg = __builtin_amdgcn_readfirstlane(hh / (H / G));
+    const size_t t0 = (size_t)bb * L + (size_t)cc * kQ;
+    dtv = dt[(t0 + t) * H + hh];
+    aSv = t < kP ? state_scale[hh * kP + t] : 0.0f;
+    crv = (t < kP && corr) ? corr[hh * kP + t] : 0.0f;
+    if constexpr (kFused) {
+      const int xo = fs.xs_per_head ? 0 : 1;
+      ax0 = fs.xs_scale[xo * (hh * kP + p0) + (1 - xo) * hh];
+      ax1 = fs.xs_scale[xo * (hh * kP + p0 + 1) + (1 - xo) * hh];
+      axs = fs.xs_scale[xo * (hh * kP + prow) + (1 - xo) * hh];
+      asp = state_scale[hh * kP + prow];
+      abq = fs.B_scale[gg];
+    }
+  };
   if constexpr (kFused) {
     // Work items in ticket order.  The sequences (b, h) are split into K blocks of consecutive
     // sequences, one per class; class x hands out its items chunk-major from its own counter, so
@@ -126,16 +156,42 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
     // dispatch over the 8 XCDs, class x runs on XCD x % 8, and the K / 8 classes of one XCD take
     // consecutive sequence blocks, so that the heads of one batch element (which share the
     // chunk's B_q^T, C_q and CB_q) meet in as few L2 caches as possible.
+    const int nbh = fs.nbh, K = fs.nclass;
+    const int q = nbh / K, r = nbh - q * K;
+    auto decode = [&](int it, int& bb, int& cc, int& hh) {
+      cc = it / nbh;
+      const int bh = it - cc * nbh;
+      bb = bh / H;
+      hh = bh - bb * H;
+    };
+    // kSpec (grids of about one round of workgroups, where every item's first loads wait in
+    // full): the item drawn when tickets follow dispatch order, the (blockIdx / K)-th ticket of
+    // class blockIdx % K, has its loads requested while the ticket is drawn (after the ticket's
+    // atomic, which they must not delay), and they are requested again only if it differs
+    int pred = -1, tk0 = 0;
+    if constexpr (kSpec) {
+      const int x = (int)(blockIdx.x & (K - 1));
+      const int sb = (x & 7) * (K >> 3) + (x >> 3);
+      const int chains = q + (sb < r ? 1 : 0);
+      const int tk = (int)(blockIdx.x / K);
+      if (chains > 0 && tk < chains * nc) {
+        const int cc = tk / chains;
+        pred = cc * nbh + sb * q + (sb < r ? sb : r) + (tk - cc * chains);
+      }
+      pred = __builtin_amdgcn_readfirstlane(pred);
+      if (t == 0) tk0 = atomicAdd(fs.sync + x * kSyncLine, 1);
+      int pb, pc, ph;
+      decode(pred < 0 ? 0 : pred, pb, pc, ph);
+      item_loads(pb, pc, ph);
+    }
     if (t == 0) {
-      const int nbh = fs.nbh, K = fs.nclass;
-      const int q = nbh / K, r = nbh - q * K;
       int item = -1;
       for (int k = 0; k < K && item < 0; ++k) {
         const int x = (int)((blockIdx.x + k) & (K - 1));
         const int sb = (x & 7) * (K >> 3) + (x >> 3);   // sequence block of class x
         const int chains = q + (sb < r ? 1 : 0);
         if (chains <= 0) continue;
-        const int tk = atomicAdd(fs.sync + x * kSyncLine, 1);
+        const int tk = (kSpec && k == 0) ? tk0 : atomicAdd(fs.sync + x * kSyncLine, 1);
         if (tk < chains * nc) {
           const int cc = tk / chains;
           item = cc * nbh + sb * q + (sb < r ? sb : r) + (tk - cc * chains);
@@ -146,17 +202,15 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
     __syncthreads();
     const int item = __builtin_amdgcn_readfirstlane(sm.misc[0]);
     if (item < 0) return;   // every item drawn (only with an uncleared counter)
-    const int nbh = fs.nbh;
-    c = item / nbh;
-    const int bh = item - c * nbh;
-    b = bh / H;
-    h = bh - b * H;
+    decode(item, b, c, h);
+    if (!kSpec || item != pred) item_loads(b, c, h);
   } else {
     const int w = xcd_remap(blockIdx.x, gridDim.x);
     h = w % H;
     const int bc = w / H;
     c = bc % nc;
     b = bc / nc;
+    item_loads(b, c, h);
   }
   // wave-uniform (the division is done on the vector unit), so that the per-group steps are
   // scalar loads and none of them drains the vector loads in flight
@@ -164,30 +218,6 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
   const size_t tok0 = (size_t)b * L + (size_t)c * kQ;
   const size_t HP = (size_t)H * kP;
   const float aCB = cb_scale[g];
-
-  // ---- loads in the order they are needed (vector loads complete in issue order): dt and the
-  //      per-channel tables first, so that the block scan and the tables wait for them alone
-  //      while the x tile is still in flight
-  float dtv = dt[(tok0 + t) * H + h];
-  const float aSv = t < kP ? state_scale[h * kP + t] : 0.0f;
-  const float crv = (t < kP && corr) ? corr[h * kP + t] : 0.0f;
-  // x tile (thread: channel pair (p0, p0+1), tokens [32 jb, 32 jb + 32))
-  const int pp = t & 31, jb = t >> 5, p0 = 2 * pp;
-  // single pass: wave -> channel tile mt and state tiles ntb, ntb + 1; lane -> channel prow
-  const int hf = lane >> 5, mt = wv & 1, ntb = (wv >> 1) * 2;
-  const int prow = mt * 32 + (lane & 31);
-  // single pass: the X_q steps of this thread's channel pair, and the step of X_q and of S_q
-  // of this lane's channel for the ChunkState requant, requested with dt (unconditional loads,
-  // so that none of the waits before them is a full drain)
-  float ax0 = 1.0f, ax1 = 1.0f, axs = 1.0f, asp = 1.0f, abq = 1.0f;
-  if constexpr (kFused) {
-    const int xo = fs.xs_per_head ? 0 : 1;
-    ax0 = fs.xs_scale[xo * (h * kP + p0) + (1 - xo) * h];
-    ax1 = fs.xs_scale[xo * (h * kP + p0 + 1) + (1 - xo) * h];
-    axs = fs.xs_scale[xo * (h * kP + prow) + (1 - xo) * h];
-    asp = state_scale[h * kP + prow];
-    abq = fs.B_scale[g];
-  }
   typename Pair<XT>::raw xr[32];
   {
     const __amdgpu_buffer_rsrc_t xrs = buffer_rsrc(x + tok0 * HP + (size_t)h * kP);
@@ -779,7 +809,7 @@ hipError_t launch_chunk_scan(const LayerDims& d, const void* x, int x_dtype, con
   if (nwork == 0) return hipSuccess;
   const dim3 grid((unsigned)nwork), block(256);
 #define SSDI8_SCAN_LAUNCH(XT, YT)                                                             \
-  hipLaunchKernelGGL((chunk_scan_kernel<XT, YT, false>), grid, block, 0, st,                  \
+  hipLaunchKernelGGL((chunk_scan_kernel<XT, YT, 0>), grid, block, 0, st,                      \
                      static_cast<const XT*>(x), dt, A, cq_frag, C_scale, c_per_token,         \
                      const_cast<int8_t*>(pin), cbq, cb_scale, state_scale, D, corr,           \
                      dt_softplus, static_cast<YT*>(y), y1_tap, d.seqlen, d.nheads, d.ngroups, \
@@ -801,16 +831,15 @@ hipError_t launch_chunk_scan_fused(const LayerDims& d, const _Float16* x, const 
   const int64_t nwork = (int64_t)d.batch * d.nchunks * d.nheads;
   if (nwork == 0) return hipSuccess;
   const dim3 grid((unsigned)nwork), block(256);
-  if (y_dtype == 1)
-    hipLaunchKernelGGL((chunk_scan_kernel<_Float16, _Float16, true>), grid, block, 0, st, x, dt,
-                       A, cq_frag, C_scale, c_per_token, pin, cbq, cb_scale, state_scale, D,
-                       corr, dt_softplus, static_cast<_Float16*>(y), nullptr, d.seqlen,
-                       d.nheads, d.ngroups, d.nchunks, fs);
-  else
-    hipLaunchKernelGGL((chunk_scan_kernel<_Float16, float, true>), grid, block, 0, st, x, dt, A,
-                       cq_frag, C_scale, c_per_token, pin, cbq, cb_scale, state_scale, D, corr,
-                       dt_softplus, static_cast<float*>(y), nullptr, d.seqlen, d.nheads,
-                       d.ngroups, d.nchunks, fs);
+#define SSDI8_FUSED_LAUNCH(YT, M)                                                                \
+  hipLaunchKernelGGL((chunk_scan_kernel<_Float16, YT, M>), grid, block, 0, st, x, dt, A, cq_frag, \
+                     C_scale, c_per_token, pin, cbq, cb_scale, state_scale, D, corr, dt_softplus, \
+                     static_cast<YT*>(y), nullptr, d.seqlen, d.nheads, d.ngroups, d.nchunks, fs)
+  if (y_dtype == 1 && fs.speculate) SSDI8_FUSED_LAUNCH(_Float16, 2);
+  else if (y_dtype == 1) SSDI8_FUSED_LAUNCH(_Float16, 1);
+  else if (fs.speculate) SSDI8_FUSED_LAUNCH(float, 2);
+  else SSDI8_FUSED_LAUNCH(float, 1);
+#undef SSDI8_FUSED_LAUNCH
   return hipGetLastError();
 }
 

@@ -97,6 +97,7 @@ struct FusedState {
   int nbh = 0;
   int nclass = 8;       // sync_classes(nbh)
   int spin_limit = 0;
+  int speculate = 0;    // request the predicted item's first loads with its ticket (small grids)
 };
 hipError_t launch_chunk_scan_fused(const LayerDims& d, const _Float16* x, const float* dt,
                                    int dt_softplus, const float* A, const int8_t* cq_frag,
