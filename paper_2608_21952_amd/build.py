@@ -32,6 +32,16 @@ FLAGS = [f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-ffp-contract=
          "-packed-fp32-ops", f"-I{INCLUDE}", f"-I{CSRC}"]
 
 
+# Per-source additions.  chunk_scan.hip: no wave-aggregated atomics, so that the single pass's
+# ticket atomic returns in the background while the loads issued after it are in flight (the
+# aggregated form reads its result, and waits for it, right away).
+SOURCE_FLAGS = {"chunk_scan.hip": ["-mllvm", "-amdgpu-atomic-optimizer-strategy=None"]}
+
+
+def flags_for(src: str) -> list:
+    return [*FLAGS, *SOURCE_FLAGS.get(src, [])]
+
+
 def hipcc() -> str:
     h = os.environ.get("HIPCC") or shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
     return h
@@ -39,7 +49,7 @@ def hipcc() -> str:
 
 def _compile(src: str) -> str:
     obj = os.path.join(OBJDIR, os.path.splitext(src)[0] + ".o")
-    cmd = [hipcc(), *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [hipcc(), *flags_for(src), "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{' '.join(cmd)}\n{r.stdout}\n{r.stderr}")

@@ -15,8 +15,8 @@ CSRC = libbuild.CSRC
 
 
 def _resources(src):
-    cmd = [libbuild.hipcc(), *libbuild.FLAGS, "-S", "--cuda-device-only", "-o", os.devnull,
-           "-Rpass-analysis=kernel-resource-usage", os.path.join(CSRC, src)]
+    cmd = [libbuild.hipcc(), *libbuild.flags_for(src), "-S", "--cuda-device-only", "-o",
+           os.devnull, "-Rpass-analysis=kernel-resource-usage", os.path.join(CSRC, src)]
     r = subprocess.run(cmd, capture_output=True, text=True)
     assert r.returncode == 0, r.stderr[-2000:]
     out, cur = {}, None
