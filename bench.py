@@ -127,12 +127,15 @@ def cpu_baseline(cfg, inp, sc, budget_s: float):
     from oracle import int8
 
     def run(nb, nh):
+        # fewer heads than the layer's stay inside group 0, so they take group 0's B, C and steps
+        ng = cfg.ngroups if nh == cfg.nheads else 1
         t = time.perf_counter()
         int8.ssdi8_forward(inp["x"][:nb, :, :nh], inp["dt_raw"][:nb, :, :nh], inp["A"][:nh],
-                           inp["B"][:nb], inp["C"][:nb], inp["D"][:nh], sc["corr"][:nh],
-                           {"alpha_B": sc["alpha_B"], "alpha_C": sc["alpha_C"],
+                           inp["B"][:nb, :, :ng], inp["C"][:nb, :, :ng], inp["D"][:nh],
+                           sc["corr"][:nh],
+                           {"alpha_B": sc["alpha_B"][:ng], "alpha_C": sc["alpha_C"][:ng],
                             "alpha_Xs": sc["alpha_Xs"][:nh], "alpha_S": sc["alpha_S"][:nh],
-                            "alpha_CB": sc["alpha_CB"]},
+                            "alpha_CB": sc["alpha_CB"][:ng]},
                            chunk=cfg.chunk, want=("y",))
         return time.perf_counter() - t
 

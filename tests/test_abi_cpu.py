@@ -275,6 +275,23 @@ def test_bench_refuses_more_than_one_gpu():
     assert r.returncode == 2 and "one GPU" in r.stderr
 
 
+@pytest.mark.parametrize("name,heads", [("mamba2-8b-g8", 16), ("mamba2-130m", 4)])
+def test_bench_cpu_baseline_samples_any_group_count(name, heads):
+    """The oracle's timed sample takes whole heads of group 0 when it cannot take every head."""
+    sys.path.insert(0, ROOT)
+    import bench
+    from oracle import calibrate
+    from paper_2608_21952_amd import synth
+    cfg = synth.CONFIGS[name].scaled(name="t", batch=2, seqlen=512, nheads=heads)
+    inp, cal = synth.draw(cfg, 1), synth.draw(cfg, 2)
+    sc = calibrate.calibrate(cal["x"], cal["dt_raw"], cal["A"], cal["B"], cal["C"], cal["D"],
+                             chunk=cfg.chunk)
+    part = bench.cpu_baseline(cfg, inp, sc, 1e-6)
+    assert part["kind"] == "oracle" and part["value"] > 0 and "heads 0.." in part["sample"]
+    whole = bench.cpu_baseline(cfg, inp, sc, 1e6)
+    assert whole["sample"].startswith("the whole workload")
+
+
 def test_calib_struct_matches_the_header(ssdi8, tmp_path):
     fields = [f[0] for f in ssdi8.CalibArgs._fields_]
     src = tmp_path / "layout_cal.c"
