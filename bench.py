@@ -118,6 +118,15 @@ def measured_traffic(kernel: str, workload: str):
     return rec.get("bytes_per_launch")
 
 
+def sample_heads(nh: int, nheads: int, ngroups: int) -> int:
+    """The head count of the oracle's sample nearest below `nh` that keeps the head-to-group
+    map: all heads, heads of group 0 only, or whole groups."""
+    hpg = nheads // ngroups
+    if nh >= nheads:
+        return nheads
+    return nh if nh <= hpg else nh - nh % hpg
+
+
 def cpu_baseline(cfg, inp, sc, budget_s: float):
     """The CPU oracle as it stands, timed on a bounded sample of the workload: the first `nh`
     heads of the first `nb` batch elements (all chunks), sized from pilots to about `budget_s`
@@ -127,8 +136,8 @@ def cpu_baseline(cfg, inp, sc, budget_s: float):
     from oracle import int8
 
     def run(nb, nh):
-        # fewer heads than the layer's stay inside group 0, so they take group 0's B, C and steps
-        ng = cfg.ngroups if nh == cfg.nheads else 1
+        # a head sample is the heads of group 0 or of whole groups 0 .. ng-1, with their B, C, steps
+        ng = cfg.ngroups if nh == cfg.nheads else -(-nh // hpg)
         t = time.perf_counter()
         int8.ssdi8_forward(inp["x"][:nb, :, :nh], inp["dt_raw"][:nb, :, :nh], inp["A"][:nh],
                            inp["B"][:nb, :, :ng], inp["C"][:nb, :, :ng], inp["D"][:nh],
@@ -144,8 +153,7 @@ def cpu_baseline(cfg, inp, sc, budget_s: float):
     pilot = run(1, 1)
     nh = int(max(1, min(cfg.nheads, budget_s / max(pilot, 1e-3))))
     nb = 1
-    if nh < cfg.nheads and G > 1:
-        nh = min(nh, hpg)                     # stay inside group 0
+    nh = sample_heads(nh, cfg.nheads, G)
     if nh == cfg.nheads:
         one = run(1, nh)
         nb = int(max(1, min(cfg.batch, budget_s / max(one, 1e-3))))

@@ -292,6 +292,14 @@ def test_bench_cpu_baseline_samples_any_group_count(name, heads):
     assert whole["sample"].startswith("the whole workload")
 
 
+def test_bench_head_sample_keeps_whole_groups():
+    sys.path.insert(0, ROOT)
+    import bench
+    assert [bench.sample_heads(n, 128, 8) for n in (1, 15, 16, 17, 40, 127, 128, 300)] == \
+        [1, 15, 16, 16, 32, 112, 128, 128]
+    assert [bench.sample_heads(n, 80, 1) for n in (1, 79, 80)] == [1, 79, 80]
+
+
 def test_calib_struct_matches_the_header(ssdi8, tmp_path):
     fields = [f[0] for f in ssdi8.CalibArgs._fields_]
     src = tmp_path / "layout_cal.c"
