@@ -94,6 +94,7 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
                          // a_CB dt_i                                   (diagonal blocks)
     float csr[kQ];       // cs_i - r_{I-1} (r_{-1} = 0), fp32
     float R[8][8];       // exp(r_a - r_b), b <= a
+    float umax[8];       // max |u_i| over block I (inf if one is NaN)
     float aS[kP];
     float cr[kP];
     double r[8];         // r_t: cs at the last token of block t
@@ -244,6 +245,10 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
     const float dtcb = aCB * dtv;
     const float u = dtcb * expf((float)(s_r[blk] - cs));
     s_u[t] = make_float2(u, -128.0f * u);
+    float um = u == u ? __builtin_fabsf(u) : __builtin_inff();
+#pragma unroll
+    for (int o = 1; o < 32; o <<= 1) um = __builtin_fmaxf(um, __shfl_xor(um, o));
+    if ((t & 31) == 0) sm.umax[blk] = um;
     const float csr = (float)(cs - rprev);
     s_csr[t] = csr;
     // the same test as the diagonal block's (on its last token's csr)
@@ -597,6 +602,24 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
       const uint32_t cbrow = frag::cb_block(jt, 0) * 1024;   // blocks (jt, it)
       const bool diag_fast =
           __builtin_amdgcn_readfirstlane((int)(s_csr[jt * 32 + 31] >= -kDiagSpan)) != 0;
+      // Leading off-diagonal blocks whose every weight rounds to an fp16 zero are skipped (the
+      // decay across the blocks between them and this row block has removed them): a weight of
+      // block it is q u_i e_j R[jt-1][it] with |q| <= 127 and e_j <= 1, below 127 2^-33 < 2^-26
+      // when max |u_i| R < 2^-33, and such a value rounds to zero.  it0 = the first block run.
+      int it0 = 0;
+      if (jt > 0) {
+        const float4 ua = *reinterpret_cast<const float4*>(sm.umax);
+        const float4 ub = *reinterpret_cast<const float4*>(sm.umax + 4);
+        const float4 ra = *reinterpret_cast<const float4*>(s_R[jt - 1]);
+        const float4 rb = *reinterpret_cast<const float4*>(s_R[jt - 1] + 4);
+        const float um[8] = {ua.x, ua.y, ua.z, ua.w, ub.x, ub.y, ub.z, ub.w};
+        const float rr[8] = {ra.x, ra.y, ra.z, ra.w, rb.x, rb.y, rb.z, rb.w};
+        uint32_t live = 1u << jt;   // the diagonal block always runs
+#pragma unroll
+        for (int k = 0; k < 7; ++k)
+          if (!(um[k] * rr[k] < 0x1p-33f)) live |= 1u << k;
+        it0 = __builtin_amdgcn_readfirstlane((int)__builtin_ctz(live));
+      }
       // W^T fragment of a 32x32 block (8 weights of this lane's token row per K-slice, as fp16)
       // times the x^T fragments of both channel tiles
       auto mfma_block = [&](const float (&wv)[8], int i0) {
@@ -623,12 +646,13 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
       // fixed register set (a copy between slots would wait for the load in flight), and every
       // load is unconditional, its block index clamped to the row's last block jt (a branch
       // around a load makes the wait after it a full drain).
-      uint4 r0 = buf_load16(cbrs, lane16, cbrow);
-      uint4 r1 = buf_load16(cbrs, lane16, cbrow + (jt < 1 ? jt : 1) * 1024);
+      auto blk = [&](int it) { return cbrow + (it < jt ? it : jt) * 1024; };
+      uint4 r0 = buf_load16(cbrs, lane16, blk(it0));
+      uint4 r1 = buf_load16(cbrs, lane16, blk(it0 + 1));
       uint4 r2;
       // off-diagonal block it < jt from slot cur; block min(it + 2, jt) into dst
       auto off_block = [&](const int it, const uint4& cur, uint4& dst) {
-        dst = buf_load16(cbrs, lane16, cbrow + (it + 2 < jt ? it + 2 : jt) * 1024);
+        dst = buf_load16(cbrs, lane16, blk(it + 2));
         // keep the prefetch at the top of the body
         __builtin_amdgcn_sched_barrier(0);
         // row factor: exp(cs_j - r_{J-1}) exp(r_{J-1} - r_I)
@@ -647,26 +671,28 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
           mfma_block(wv, i0);
         }
       };
-      if (jt > 0) {
-        off_block(0, r0, r2);
-        if (jt > 1) {
-          off_block(1, r1, r0);
-          if (jt > 2) {
-            off_block(2, r2, r1);
-            if (jt > 3) {
-              off_block(3, r0, r2);
-              if (jt > 4) {
-                off_block(4, r1, r0);
-                if (jt > 5) {
-                  off_block(5, r2, r1);
-                  if (jt > 6) off_block(6, r0, r2);
+      // block it0 + k sits in slot k % 3
+      const int nb = jt - it0;
+      if (nb > 0) {
+        off_block(it0, r0, r2);
+        if (nb > 1) {
+          off_block(it0 + 1, r1, r0);
+          if (nb > 2) {
+            off_block(it0 + 2, r2, r1);
+            if (nb > 3) {
+              off_block(it0 + 3, r0, r2);
+              if (nb > 4) {
+                off_block(it0 + 4, r1, r0);
+                if (nb > 5) {
+                  off_block(it0 + 5, r2, r1);
+                  if (nb > 6) off_block(it0 + 6, r0, r2);
                 }
               }
             }
           }
         }
       }
-      const int js = jt % 3;
+      const int js = nb % 3;
       const uint4 cur = js == 0 ? r0 : (js == 1 ? r1 : r2);
       // the C_q fragments of ChunkScan1, in flight during the diagonal block
       {
@@ -703,9 +729,13 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
         mfma_block(wv, i0);
       }
     }
-    // -- Scan1: Y1^T = P_in . C_q^T, int8 MFMA over n
+    // -- Scan1: Y1^T = P_in . C_q^T, int8 MFMA over n.  Its term is Y1 a_C exp(cs_j) a_S[p];
+    //    when exp(r_{J-1}) is zero in fp32 every factor exp(cs_j) of the block is a zero
+    //    product and Y1 is not needed (unless it is tapped)
+    const float er = jt ? __expf((float)s_r[jt - 1]) : 1.0f;
+    const bool need_y1 = y1_tap || __builtin_amdgcn_readfirstlane((int)(er != 0.0f)) != 0;
     v16i yi0 = {}, yi1 = {};
-    {
+    if (need_y1) {
       // the P_in fragments are the same for both j-blocks; an opaque offset makes each call
       // load them again (from L2) instead of holding 32 registers across the other block
       uint32_t lofs = lane16;
@@ -724,7 +754,7 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
     }
     // -- epilogue of token row jrow: y = Y1 a_C exp(cs_j) a_S[p] + (y_diag + D x + corr[p])
     // a_C(j) exp(cs_j) = a_C(j) exp(cs_j - r_{J-1}) exp(r_{J-1})
-    const float eo = ac * ej * (jt ? __expf((float)s_r[jt - 1]) : 1.0f);
+    const float eo = ac * ej * er;
 #pragma unroll
     for (int pt = 0; pt < 2; ++pt) {
 #pragma unroll

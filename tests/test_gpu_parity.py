@@ -164,6 +164,30 @@ def _small(name="variant", **kw):
     return synth.CONFIGS["mamba2-130m"].scaled(**base)
 
 
+def test_decay_skips_leave_y_unchanged(torch, ssdi8):
+    """ChunkScan1 of a 32-token block whose decay factor exp(cs) is zero in fp32 is skipped
+    unless its INT32 product is tapped: y must be bit-identical with and without the tap (a
+    tapped call runs the separate kernels, so the single pass is held to them too).  The inputs
+    decay strongly enough that both ChunkScan skips (that one, and off-diagonal blocks of the
+    fp16 weights that round to zero) occur."""
+    cfg = _small("decay-skip", batch=1, seqlen=1024, nheads=8, ngroups=1)
+    say(f"layer {cfg.name}")
+    inp = synth.draw(cfg, 1)
+    sc = calibration(cfg)
+    dt = np.log1p(np.exp(inp["dt_raw"].astype(np.float64)))
+    cs = np.cumsum((dt * inp["A"].astype(np.float64)).reshape(1, -1, cfg.chunk, 8), axis=2)
+    ends = cs[:, :, 31:-1:32]                       # cs at the last token of blocks 0..6
+    assert (ends < -110).any() and (ends > -80).any()
+    for path in ("separate", "single"):
+        plain = run_layer(torch, ssdi8, inp, sc, path=path)
+        tapped = run_layer(torch, ssdi8, inp, sc, path=path, taps=("scan1_i32",))
+        assert np.array_equal(plain["y"].view(np.uint16), tapped["y"].view(np.uint16)), path
+        assert np.array_equal(plain["final_state_q"], tapped["final_state_q"]), path
+    ref = oq.ssdi8_forward(inp["x"], inp["dt_raw"], inp["A"], inp["B"], inp["C"], inp["D"],
+                           sc["corr"], sc, chunk=cfg.chunk, want=("y",))
+    assert_close(plain["y"], ref["y"], "y (whole layer)")
+
+
 def test_layer_per_head_xs_scale(torch, ssdi8):
     cfg = _small("per-head", xs_per_head=True)
     say(f"layer {cfg.name}")
