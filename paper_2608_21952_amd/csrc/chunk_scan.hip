@@ -373,7 +373,7 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
     constexpr int kPolicySc1 = 16;
     const int bh = b * H + h;
     int* flags = fs.sync + kSyncFlags + (size_t)bh * nc;   // flag of chunk m at flags[m]
-    const int qd = sm.misc[1];
+    const int qd = __builtin_amdgcn_readfirstlane(sm.misc[1]);
     auto slab_of = [&](int8_t* base, int cc) {
       return base + (((size_t)b * nc + cc) * H + h) * kSlab;
     };
@@ -428,6 +428,20 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
     };
     const uint4 sq0 = make_uint4(sq[0][0], sq[0][1], sq[0][2], sq[0][3]);
     const uint4 sq1 = make_uint4(sq[1][0], sq[1][1], sq[1][2], sq[1][3]);
+    // With Q(Decay) = 0, Eq. 9 gives P_in[c+1] = clamp(S_q[c] + (r >> k)) whatever P_in[c] is:
+    // such a chunk publishes P_in[c+1] before it obtains P_in[c], so that its successor finds
+    // an anchor at once (the same integers; its S_q is then never needed by later chunks)
+    const bool early = qd == 0 && c + 1 < nc;
+    if (early) {
+      const uint4 z = make_uint4(0u, 0u, 0u, 0u);
+      int8_t* slab = slab_of(pin, c + 1);
+      st_sc1(step(z, sq0, 0), slab, off0);
+      st_sc1(step(z, sq1, 0), slab, off1);
+      __builtin_amdgcn_s_waitcnt(0);
+      __syncthreads();
+      if (t == 0)
+        __hip_atomic_store(flags + c, (int)kFlagP, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
     uint4 p0, p1;   // P_in[c]
     if (c == 0) {
       // the initial state (row-major; 0 without one), also ChunkScan1's entering state of chunk 0
@@ -455,14 +469,17 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
       __syncthreads();
       int l = __builtin_amdgcn_readfirstlane(sm.misc[2]);
       if (l < 0) {
-        // publish S_q[c] for the chunks after this one, then wait for an anchor
-        int8_t* sslab = slab_of(fs.sq, c);
-        st_sc1(sq0, sslab, off0);
-        st_sc1(sq1, sslab, off1);
-        __builtin_amdgcn_s_waitcnt(0);
-        __syncthreads();
+        // publish S_q[c] for the chunks after this one (unless P_in[c+1] already is), then wait
+        // for an anchor
+        if (!early) {
+          int8_t* sslab = slab_of(fs.sq, c);
+          st_sc1(sq0, sslab, off0);
+          st_sc1(sq1, sslab, off1);
+          __builtin_amdgcn_s_waitcnt(0);
+          __syncthreads();
+        }
         if (wv == 0) {
-          if (lane == 0)
+          if (lane == 0 && !early)
             __hip_atomic_store(flags + c, (int)(kFlagS | (uint32_t)qd), __ATOMIC_RELAXED,
                                __HIP_MEMORY_SCOPE_AGENT);
           uint32_t f = 0;
@@ -516,9 +533,11 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
     // P_in[c+1] = clamp(S_q[c] + ((q_d P_in[c] + r) >> k))
     const uint4 n0 = step(p0, sq0, qd), n1 = step(p1, sq1, qd);
     if (c + 1 < nc) {
-      int8_t* slab = slab_of(pin, c + 1);
-      st_sc1(n0, slab, off0);
-      st_sc1(n1, slab, off1);
+      if (!early) {
+        int8_t* slab = slab_of(pin, c + 1);
+        st_sc1(n0, slab, off0);
+        st_sc1(n1, slab, off1);
+      }
     } else {
       const float a = s_aS[prow];   // state_scale[h, prow], staged in LDS at the start
       const uint32_t nw[2][4] = {{n0.x, n0.y, n0.z, n0.w}, {n1.x, n1.y, n1.z, n1.w}};
@@ -537,7 +556,7 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
     }
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    if (t == 0 && c + 1 < nc)
+    if (t == 0 && c + 1 < nc && !early)
       __hip_atomic_store(flags + c, (int)(kFlagP | (uint32_t)qd), __ATOMIC_RELAXED,
                          __HIP_MEMORY_SCOPE_AGENT);
   };
