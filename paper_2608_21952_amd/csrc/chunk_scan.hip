@@ -299,8 +299,14 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
       for (int i = 0; i < 4; ++i) {
         const int r = 4 * r4 + i;
         const float lut = sm.lut[jb * 32 + r];
-        qa[i] = quant_bits(lut * (float)__builtin_bit_cast(_Float16, Pair<XT>::lo(xr[r])), inv0);
-        qb[i] = quant_bits(lut * (float)__builtin_bit_cast(_Float16, Pair<XT>::hi(xr[r])), inv1);
+        // fl32(lut x) as one mixed-precision fma with +0 (only a zero product's sign can
+        // differ, and it quantizes to 0 either way)
+        qa[i] = quant_bits(
+            __builtin_fmaf(lut, (float)__builtin_bit_cast(_Float16, Pair<XT>::lo(xr[r])), 0.0f),
+            inv0);
+        qb[i] = quant_bits(
+            __builtin_fmaf(lut, (float)__builtin_bit_cast(_Float16, Pair<XT>::hi(xr[r])), 0.0f),
+            inv1);
       }
       w0[r4] = pack_lo4(qa[0], qa[1], qa[2], qa[3]);
       w1[r4] = pack_lo4(qb[0], qb[1], qb[2], qb[3]);
@@ -433,10 +439,12 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
     // an anchor at once (the same integers; its S_q is then never needed by later chunks)
     const bool early = qd == 0 && c + 1 < nc;
     if (early) {
+      // r < 2^k (r = 2^(k-1) or 0) makes it S_q[c] itself (codes within +-127)
+      const bool same = (fs.radd >> fs.shift) == 0;
       const uint4 z = make_uint4(0u, 0u, 0u, 0u);
       int8_t* slab = slab_of(pin, c + 1);
-      st_sc1(step(z, sq0, 0), slab, off0);
-      st_sc1(step(z, sq1, 0), slab, off1);
+      st_sc1(same ? sq0 : step(z, sq0, 0), slab, off0);
+      st_sc1(same ? sq1 : step(z, sq1, 0), slab, off1);
       __builtin_amdgcn_s_waitcnt(0);
       __syncthreads();
       if (t == 0)
@@ -531,14 +539,14 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
       }
     }
     // P_in[c+1] = clamp(S_q[c] + ((q_d P_in[c] + r) >> k))
-    const uint4 n0 = step(p0, sq0, qd), n1 = step(p1, sq1, qd);
     if (c + 1 < nc) {
       if (!early) {
         int8_t* slab = slab_of(pin, c + 1);
-        st_sc1(n0, slab, off0);
-        st_sc1(n1, slab, off1);
+        st_sc1(step(p0, sq0, qd), slab, off0);
+        st_sc1(step(p1, sq1, qd), slab, off1);
       }
     } else {
+      const uint4 n0 = step(p0, sq0, qd), n1 = step(p1, sq1, qd);
       const float a = s_aS[prow];   // state_scale[h, prow], staged in LDS at the start
       const uint32_t nw[2][4] = {{n0.x, n0.y, n0.z, n0.w}, {n1.x, n1.y, n1.z, n1.w}};
 #pragma unroll
