@@ -95,6 +95,7 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
     float csr[kQ];       // cs_i - r_{I-1} (r_{-1} = 0), fp32
     float R[8][8];       // exp(r_a - r_b), b <= a
     float umax[8];       // max |u_i| over block I (inf if one is NaN)
+    int it0[8];          // single pass: the first ChunkScan2 block run by row block J
     float aS[kP];
     float cr[kP];
     double r[8];         // r_t: cs at the last token of block t
@@ -358,6 +359,23 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
     __syncthreads();
   }
 
+  // The first off-diagonal ChunkScan2 block that row block jt runs: leading blocks whose every
+  // fp16 weight rounds to zero are skipped (see the j-block).  jt itself when all are skipped.
+  auto first_block = [&](int jt) {
+    if (jt <= 0) return 0;
+    const float4 ua = *reinterpret_cast<const float4*>(sm.umax);
+    const float4 ub = *reinterpret_cast<const float4*>(sm.umax + 4);
+    const float4 ra = *reinterpret_cast<const float4*>(s_R[jt - 1]);
+    const float4 rb = *reinterpret_cast<const float4*>(s_R[jt - 1] + 4);
+    const float um[8] = {ua.x, ua.y, ua.z, ua.w, ub.x, ub.y, ub.z, ub.w};
+    const float rr[8] = {ra.x, ra.y, ra.z, ra.w, rb.x, rb.y, rb.z, rb.w};
+    uint32_t live = 1u << jt;   // the diagonal block always runs
+#pragma unroll
+    for (int k = 0; k < 7; ++k)
+      if (!(um[k] * rr[k] < 0x1p-33f)) live |= 1u << k;
+    return (int)__builtin_ctz(live);
+  };
+
   // ---- single pass, StatePassing (Eq. 9) for this chunk.  P_in[c], the state entering the
   //      chunk, comes from the chunks before it in its sequence.  The flag word of chunk m holds
   //      its Q(Decay) in the low 16 bits and two status bits: kFlagS (its chunk-local S_q is in
@@ -375,6 +393,9 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
   //      are written and read at the agent's coherence point (sc1) and are complete before
   //      their flag is set.
   auto hand_off = [&]() {
+    // the first ChunkScan2 block of each row block, for the j-blocks after the hand-off's last
+    // barrier (the tables are complete)
+    if (wv == 0 && lane < 8) sm.it0[lane] = first_block(lane);
     constexpr size_t kSlab = (size_t)kP * kN;
     constexpr int kPolicySc1 = 16;
     const int bh = b * H + h;
@@ -634,18 +655,10 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
       // block it is q u_i e_j R[jt-1][it] with |q| <= 127 and e_j <= 1, below 127 2^-33 < 2^-26
       // when max |u_i| R < 2^-33, and such a value rounds to zero.  it0 = the first block run.
       int it0 = 0;
-      if (jt > 0) {
-        const float4 ua = *reinterpret_cast<const float4*>(sm.umax);
-        const float4 ub = *reinterpret_cast<const float4*>(sm.umax + 4);
-        const float4 ra = *reinterpret_cast<const float4*>(s_R[jt - 1]);
-        const float4 rb = *reinterpret_cast<const float4*>(s_R[jt - 1] + 4);
-        const float um[8] = {ua.x, ua.y, ua.z, ua.w, ub.x, ub.y, ub.z, ub.w};
-        const float rr[8] = {ra.x, ra.y, ra.z, ra.w, rb.x, rb.y, rb.z, rb.w};
-        uint32_t live = 1u << jt;   // the diagonal block always runs
-#pragma unroll
-        for (int k = 0; k < 7; ++k)
-          if (!(um[k] * rr[k] < 0x1p-33f)) live |= 1u << k;
-        it0 = __builtin_amdgcn_readfirstlane((int)__builtin_ctz(live));
+      if constexpr (kFused) {
+        it0 = __builtin_amdgcn_readfirstlane(sm.it0[jt]);   // formed by the hand-off
+      } else if (jt > 0) {
+        it0 = __builtin_amdgcn_readfirstlane(first_block(jt));
       }
       // W^T fragment of a 32x32 block (8 weights of this lane's token row per K-slice, as fp16)
       // times the x^T fragments of both channel tiles
@@ -760,7 +773,8 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
     //    when exp(r_{J-1}) is zero in fp32 every factor exp(cs_j) of the block is a zero
     //    product and Y1 is not needed (unless it is tapped)
     const float er = jt ? __expf((float)s_r[jt - 1]) : 1.0f;
-    const bool need_y1 = y1_tap || __builtin_amdgcn_readfirstlane((int)(er != 0.0f)) != 0;
+    const bool tap_y1 = !kFused && y1_tap;   // the single pass has no Y1 tap
+    const bool need_y1 = tap_y1 || __builtin_amdgcn_readfirstlane((int)(er != 0.0f)) != 0;
     v16i yi0 = {}, yi1 = {};
     if (need_y1) {
       // the P_in fragments are the same for both j-blocks; an opaque offset makes each call
@@ -798,7 +812,7 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
           const float yd = pt ? yd1[r] : yd0[r];
           v[q] = __builtin_fmaf((float)yi[q] * eo, asv[q], yd);
         }
-        if (y1_tap)
+        if (tap_y1)
           *reinterpret_cast<int4*>(y1_tap + orow + pb) = make_int4(yi[0], yi[1], yi[2], yi[3]);
         if constexpr (sizeof(YT) == 4) {
           *reinterpret_cast<float4*>(y + orow + pb) = make_float4(v[0], v[1], v[2], v[3]);
