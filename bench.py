@@ -338,6 +338,9 @@ def main():
                          "workload (65536 tokens x 80 heads)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget-s", type=float, default=15.0)
+    ap.add_argument("--settle-s", type=float, default=0.3,
+                    help="untimed steps after the warmup until the GPU has run the layer this "
+                         "long (its clocks reach steady state under sustained load)")
     ap.add_argument("--eager", action="store_true",
                     help="time eager launches instead of replays of one captured HIP graph")
     ap.add_argument("--path", choices=("auto", "separate", "single"), default="auto",
@@ -424,6 +427,19 @@ def main():
             step()
         for _ in range(W):
             graph.replay()
+        torch.cuda.synchronize()
+    # Settle: untimed steps until the GPU has run the layer for args.settle_s seconds.  Under
+    # sustained load its clocks take tens of ms to reach steady state (2.7B-shaped layer, 10
+    # steps per sample: 0.148, 0.165, 0.169, 0.164, 0.161, ... 0.141 ms per step by the 250th).
+    settle_end = time.perf_counter() + args.settle_s
+    settle_steps = 0
+    while time.perf_counter() < settle_end:
+        for _ in range(10):
+            if graph is not None:
+                graph.replay()
+            else:
+                step()
+        settle_steps += 10
         torch.cuda.synchronize()
     t0 = torch.cuda.Event(enable_timing=True)
     t1 = torch.cuda.Event(enable_timing=True)
@@ -521,6 +537,9 @@ def main():
                      "avg_us": round(per[dom] * 1e3, 2)},
         "timing": ("K replays of one captured HIP graph; per-kernel times from K eager steps "
                    "bracketed by HIP events" if graph is not None else "eager launches"),
+        "settle": {"seconds": args.settle_s, "steps": settle_steps,
+                   "what": "untimed steps after the warmup, until the GPU has run the layer "
+                           "this long (clocks at steady state)"},
         "layer_hbm_frac": round(layer_min_bytes(cfg) / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "path": ("single pass: ChunkBMM, then ChunkState + StatePassing + ChunkScan in one kernel"
                  if single else "separate ChunkBMM, ChunkState, StatePassing, ChunkScan kernels")
