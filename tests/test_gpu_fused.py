@@ -89,6 +89,12 @@ CASES = [
     _small("fused-groups", nheads=6, ngroups=3, seqlen=1536),
     _small("fused-per-head", xs_per_head=True, seqlen=768),
     _small("fused-one-chunk", seqlen=256, batch=3),
+    # slowly decaying heads (A in [-0.14, -0.018]): Q(Decay) > 0 on every chunk, so every
+    # entering state comes through the look-back hand-off
+    _small("fused-slow-decay", seqlen=2048, a_lo=-4.0, a_hi=-2.0),
+    # the 64K-token layer's mix (A in [-16, -0.018]): early zero-decay publications and
+    # look-back chains side by side
+    _small("fused-mixed-decay", seqlen=2048, nheads=16, a_lo=-4.0),
 ]
 
 
