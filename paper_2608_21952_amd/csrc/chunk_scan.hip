@@ -18,6 +18,8 @@
 // second factor to stay finite; otherwise it evaluates exp per element.
 //
 // Work split: wave w owns the j-blocks {w, 7-w} (1+w + 8-w = 9 causal block pairs per wave).
+// Strong decay removes work exactly: leading off-diagonal blocks whose fp16 weights all round to
+// zero are not formed, and Scan1 is not run for a j-block whose factor exp(cs_j) is zero in fp32.
 // x is staged once in LDS as x^T [p][i] (fp16, tokens contiguous = the Scan2 MFMA K-slice); the
 // D skip term reads it back per token, and the fp16 output leaves through the same bytes as whole
 // 128-byte rows.  C_q, P_in and CB_q arrive in MFMA fragment order (frag.hpp), so every operand
