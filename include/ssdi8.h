@@ -163,9 +163,9 @@ typedef struct {
      sequence through the workspace (a flag per chunk; Eq. 9 applied in chunk order, so every
      integer result and y are bit-identical to the separate kernels).  The state_in_q tap is
      served by either path.  0: automatic (the single pass where it is the faster one, which
-     takes enough concurrent sequences to hide the serial hand-offs: batch * nheads >= 192 with
-     at least 4 chunks, >= 128 with at least 16, or >= 80 with at least 32); 1: always the
-     separate kernels; 2: the single pass whenever eligible.
+     takes enough concurrent sequences to hide the serial hand-offs: batch * nheads >= 72 with
+     at least 4 chunks, or >= 48 with at least 32); 1: always the separate kernels; 2: the
+     single pass whenever eligible.
      With the single pass, events 1-3 of stage_events are recorded back to back before it. */
   int path;
   /* Alternative to Bq / Cq (both NULL then): the unquantized B, C [B,L,G,N] of bc_dtype

@@ -174,12 +174,13 @@ bool single_pass(const ssdi8_dims* d, const ssdi8_scan_args* a) {
                         !a->state_q && !a->decay_q && !a->scan1_i32;
   if (!eligible) return false;
   if (a->path != 0) return a->path == 2;
-  // automatic: the single pass hides its chain of nc hand-offs behind enough concurrent
-  // sequences; measured crossover on MI355X (130M-shaped layers, B H sequences of nc chunks):
-  // it wins from 192 sequences at 4 chunks, from 128 at 16 and from 80 at 32 and more
+  // automatic: the single pass hides its chains of hand-offs behind enough concurrent sequences.
+  // Measured crossover on MI355X (130M-shaped layers, B H sequences of nc chunks), taken where
+  // the chains are longest (slowly decaying heads, no chunk with a zero Q(Decay)): it wins from
+  // 72 sequences at 4 chunks and more, and from 48 sequences at 32 chunks
   const int64_t nc = d->chunk > 0 ? d->seqlen / d->chunk : 0;
   const int64_t bh = d->batch * d->nheads;
-  return (bh >= 192 && nc >= 4) || (bh >= 128 && nc >= 16) || (bh >= 80 && nc >= 32);
+  return (bh >= 72 && nc >= 4) || (bh >= 48 && nc >= 32);
 }
 
 }  // namespace

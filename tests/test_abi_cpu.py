@@ -364,16 +364,18 @@ def test_single_pass_selection(ssdi8):
     f16, f32 = torch.float16, torch.float32
     use = lambda dd, *a, **k: ssdi8.uses_single_pass(dd, *a, **k)
     assert use(ssdi8.dims(8, 2048, 24, 1), f16)                # 192 sequences of 8 chunks
-    assert not use(ssdi8.dims(4, 2048, 24, 1), f16)            # 96 sequences of 8 chunks
+    assert use(ssdi8.dims(4, 2048, 24, 1), f16)                # 96 sequences of 8 chunks
+    assert use(ssdi8.dims(3, 1024, 24, 1), f16)                # 72 sequences of 4 chunks
+    assert not use(ssdi8.dims(3, 768, 24, 1), f16)             # 72 sequences of 3 chunks
     assert not use(ssdi8.dims(8, 512, 24, 1), f16)             # 2 chunks
-    assert use(ssdi8.dims(4, 4096, 32, 1), f16)                # 128 sequences of 16 chunks
-    assert not use(ssdi8.dims(4, 2048, 32, 1), f16)            # 128 sequences of 8 chunks
+    assert not use(ssdi8.dims(2, 4096, 24, 1), f16)            # 48 sequences of 16 chunks
+    assert use(ssdi8.dims(2, 8192, 24, 1), f16)                # 48 sequences of 32 chunks
+    assert not use(ssdi8.dims(1, 65536, 24, 1), f16)           # 24 sequences: chain-bound
     assert use(ssdi8.dims(4, 4096, 80, 1), f16)                # 16 chunks, 320 sequences
     assert use(ssdi8.dims(2, 8192, 128, 8), f16)
     assert use(ssdi8.dims(1, 65536, 80, 1), f16)               # 80 sequences of 256 chunks
-    assert use(ssdi8.dims(1, 16384, 80, 1), f16)               # 80 sequences of 64 chunks
-    assert not use(ssdi8.dims(1, 4096, 96, 1), f16)            # 96 sequences of 16 chunks
-    assert not use(ssdi8.dims(1, 65536, 48, 1), f16)           # 48 sequences: chain-bound
+    assert use(ssdi8.dims(1, 4096, 96, 1), f16)                # 96 sequences of 16 chunks
+    assert not use(ssdi8.dims(1, 4096, 40, 1), f16)            # 40 sequences of 16 chunks
     assert use(ssdi8.dims(8, 2048, 24, 1), f16, "single")
     assert not use(ssdi8.dims(4, 4096, 80, 1), f16, "separate")
     assert not use(ssdi8.dims(4, 4096, 80, 1), f32, "single")  # fp32 x: separate kernels
