@@ -358,6 +358,7 @@ ssdi8_status ssdi8_ssd_chunk_scan(const ssdi8_dims* d, const ssdi8_scan_args* a,
     // full, so they are requested with the ticket for the item dispatch order predicts
     const int64_t nitems = (int64_t)ld.batch * ld.nchunks * ld.nheads;
     fs.speculate = nitems <= (int64_t)8 * device_cus() ? 1 : 0;
+    fs.stream = ssdi8::stream_xy(ld, 2, a->y_dtype == SSDI8_F16 ? 2 : 4);
     e = ssdi8::launch_chunk_scan_fused(ld, static_cast<const _Float16*>(a->x), a->dt,
                                        a->dt_softplus, a->A, cq, a->C_scale, a->c_per_token, pin,
                                        cbq, a->cb_scale, a->state_scale, a->D, a->corr, a->y,
@@ -382,7 +383,10 @@ ssdi8_status ssdi8_ssd_chunk_scan(const ssdi8_dims* d, const ssdi8_scan_args* a,
   if (e != hipSuccess || !mark(3)) return SSDI8_ERR_HIP;
   e = ssdi8::launch_chunk_scan(ld, a->x, a->x_dtype, a->dt, a->dt_softplus, a->A, cq,
                                a->C_scale, a->c_per_token, pin, cbq, a->cb_scale, a->state_scale,
-                               a->D, a->corr, a->y, a->y_dtype, a->scan1_i32, st);
+                               a->D, a->corr, a->y, a->y_dtype, a->scan1_i32,
+                               ssdi8::stream_xy(ld, a->x_dtype == SSDI8_F16 ? 2 : 4,
+                                                a->y_dtype == SSDI8_F16 ? 2 : 4),
+                               st);
   if (e != hipSuccess || !mark(4)) return SSDI8_ERR_HIP;
   return SSDI8_OK;
 }

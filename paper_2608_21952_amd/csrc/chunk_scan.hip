@@ -49,16 +49,18 @@ constexpr uint32_t kFlagP = 1u << 17;   // the state entering the next chunk is 
 template <typename XT> struct Pair;
 template <> struct Pair<_Float16> {
   typedef uint32_t raw;
+  template <int kPol = 0>
   static __device__ __forceinline__ raw load(__amdgpu_buffer_rsrc_t r, uint32_t vo, uint32_t so) {
-    return buf_load4(r, vo, so);
+    return buf_load4<kPol>(r, vo, so);
   }
   static __device__ __forceinline__ uint16_t lo(raw v) { return (uint16_t)(v & 0xffffu); }
   static __device__ __forceinline__ uint16_t hi(raw v) { return (uint16_t)(v >> 16); }
 };
 template <> struct Pair<float> {
   typedef float2 raw;
+  template <int kPol = 0>
   static __device__ __forceinline__ raw load(__amdgpu_buffer_rsrc_t r, uint32_t vo, uint32_t so) {
-    const uint2 v = buf_load8(r, vo, so);
+    const uint2 v = buf_load8<kPol>(r, vo, so);
     return make_float2(__uint_as_float(v.x), __uint_as_float(v.y));
   }
   static __device__ __forceinline__ uint16_t lo(raw v) {
@@ -226,8 +228,16 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
   {
     const __amdgpu_buffer_rsrc_t xrs = buffer_rsrc(x + tok0 * HP + (size_t)h * kP);
     const uint32_t xo = (uint32_t)((jb * 32 * HP + p0) * sizeof(XT));
+    // x and y are touched once: streamed (non-temporal) when the layer's x and y exceed the
+    // Infinity Cache, so that they do not displace the tiles every head of a chunk reuses
+    if (fs.stream) {
 #pragma unroll
-    for (int r = 0; r < 32; ++r) xr[r] = Pair<XT>::load(xrs, xo, (uint32_t)(r * HP * sizeof(XT)));
+      for (int r = 0; r < 32; ++r)
+        xr[r] = Pair<XT>::template load<kPolicyNT>(xrs, xo, (uint32_t)(r * HP * sizeof(XT)));
+    } else {
+#pragma unroll
+      for (int r = 0; r < 32; ++r) xr[r] = Pair<XT>::load(xrs, xo, (uint32_t)(r * HP * sizeof(XT)));
+    }
   }
   // ---- ChunkCumsum (fp64 sums; the factors derived from it only need fp32 accuracy here).
   //      dt is the fp64 softplus rounded once to fp32, as in ChunkState: one dt per token for
@@ -862,10 +872,17 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
       const uint8_t* src = s_y + jt8 * 128 + ((col ^ (jt8 & 7)) * 16);
       const __amdgpu_buffer_rsrc_t yrs = buffer_rsrc(y + tok0 * HP + (size_t)h * kP);
       const uint32_t yo = (uint32_t)(jt8 * HP * 2 + col * 16);
+      if (fs.stream) {
 #pragma unroll
-      for (int k = 0; k < (kQ * kP * 2) / (16 * 256); ++k)
-        buf_store16(*reinterpret_cast<const uint4*>(src + k * 32 * 128), yrs, yo,
-                    (uint32_t)(k * 32 * HP * 2));
+        for (int k = 0; k < (kQ * kP * 2) / (16 * 256); ++k)
+          buf_store16<kPolicyNT>(*reinterpret_cast<const uint4*>(src + k * 32 * 128), yrs, yo,
+                                 (uint32_t)(k * 32 * HP * 2));
+      } else {
+#pragma unroll
+        for (int k = 0; k < (kQ * kP * 2) / (16 * 256); ++k)
+          buf_store16(*reinterpret_cast<const uint4*>(src + k * 32 * 128), yrs, yo,
+                      (uint32_t)(k * 32 * HP * 2));
+      }
     }
   }
 }
@@ -877,16 +894,18 @@ hipError_t launch_chunk_scan(const LayerDims& d, const void* x, int x_dtype, con
                              const float* C_scale, int c_per_token, const int8_t* pin,
                              const int8_t* cbq, const float* cb_scale, const float* state_scale,
                              const float* D, const float* corr, void* y, int y_dtype,
-                             int32_t* y1_tap, hipStream_t st) {
+                             int32_t* y1_tap, int stream, hipStream_t st) {
   const int64_t nwork = (int64_t)d.batch * d.nchunks * d.nheads;
   if (nwork == 0) return hipSuccess;
   const dim3 grid((unsigned)nwork), block(256);
+  FusedState fs;
+  fs.stream = stream;
 #define SSDI8_SCAN_LAUNCH(XT, YT)                                                             \
   hipLaunchKernelGGL((chunk_scan_kernel<XT, YT, 0>), grid, block, 0, st,                      \
                      static_cast<const XT*>(x), dt, A, cq_frag, C_scale, c_per_token,         \
                      const_cast<int8_t*>(pin), cbq, cb_scale, state_scale, D, corr,           \
                      dt_softplus, static_cast<YT*>(y), y1_tap, d.seqlen, d.nheads, d.ngroups, \
-                     d.nchunks, FusedState{})
+                     d.nchunks, fs)
   if (x_dtype == 1 && y_dtype == 1) SSDI8_SCAN_LAUNCH(_Float16, _Float16);
   else if (x_dtype == 1) SSDI8_SCAN_LAUNCH(_Float16, float);
   else if (y_dtype == 1) SSDI8_SCAN_LAUNCH(float, _Float16);

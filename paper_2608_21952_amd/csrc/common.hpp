@@ -32,20 +32,26 @@ __device__ __forceinline__ uint4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t v
   const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, (int)soff, 0);
   return make_uint4(v[0], v[1], v[2], v[3]);
 }
+// Cache policy of a buffer access (gfx950): 0 the default; kPolicyNT non-temporal, for data a
+// kernel touches once (streamed through the caches instead of displacing what is reused).
+constexpr int kPolicyNT = 2;
+template <int kPol = 0>
 __device__ __forceinline__ uint2 buf_load8(__amdgpu_buffer_rsrc_t r, uint32_t voff,
                                            uint32_t soff) {
-  const auto v = __builtin_amdgcn_raw_buffer_load_b64(r, (int)voff, (int)soff, 0);
+  const auto v = __builtin_amdgcn_raw_buffer_load_b64(r, (int)voff, (int)soff, kPol);
   return make_uint2(v[0], v[1]);
 }
+template <int kPol = 0>
 __device__ __forceinline__ uint32_t buf_load4(__amdgpu_buffer_rsrc_t r, uint32_t voff,
                                               uint32_t soff) {
-  return __builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, (int)soff, 0);
+  return __builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, (int)soff, kPol);
 }
+template <int kPol = 0>
 __device__ __forceinline__ void buf_store16(uint4 d, __amdgpu_buffer_rsrc_t r, uint32_t voff,
                                             uint32_t soff) {
   typedef uint32_t u32x4 __attribute__((vector_size(16)));
   const u32x4 v = {d.x, d.y, d.z, d.w};
-  __builtin_amdgcn_raw_buffer_store_b128(v, r, (int)voff, (int)soff, 0);
+  __builtin_amdgcn_raw_buffer_store_b128(v, r, (int)voff, (int)soff, kPol);
 }
 
 // Symmetric int8 quantization of an fp32 value with a precomputed inverse step:

@@ -20,16 +20,18 @@ static_assert(kP * kXTS >= kQ * kP * 2, "the fp16 output stage reuses the x^T by
 template <typename XT> struct Pair;
 template <> struct Pair<_Float16> {
   typedef uint32_t raw;
+  template <int kPol = 0>
   static __device__ __forceinline__ raw load(__amdgpu_buffer_rsrc_t r, uint32_t vo, uint32_t so) {
-    return buf_load4(r, vo, so);
+    return buf_load4<kPol>(r, vo, so);
   }
   static __device__ __forceinline__ uint16_t lo(raw v) { return (uint16_t)(v & 0xffffu); }
   static __device__ __forceinline__ uint16_t hi(raw v) { return (uint16_t)(v >> 16); }
 };
 template <> struct Pair<float> {
   typedef float2 raw;
+  template <int kPol = 0>
   static __device__ __forceinline__ raw load(__amdgpu_buffer_rsrc_t r, uint32_t vo, uint32_t so) {
-    const uint2 v = buf_load8(r, vo, so);
+    const uint2 v = buf_load8<kPol>(r, vo, so);
     return make_float2(__uint_as_float(v.x), __uint_as_float(v.y));
   }
   static __device__ __forceinline__ uint16_t lo(raw v) {
@@ -62,7 +64,7 @@ __global__ __launch_bounds__(256, 3) void fp16_scan_kernel(
     const XT* __restrict__ x, const float* __restrict__ dt, const float* __restrict__ A,
     const _Float16* __restrict__ c_frag, const float* __restrict__ pin,
     const float* __restrict__ cb, const float* __restrict__ Dv, int dt_softplus,
-    YT* __restrict__ y, int L, int H, int G, int nc) {
+    YT* __restrict__ y, int L, int H, int G, int nc, int stream) {
   struct __attribute__((aligned(16))) Smem {
     float u[kQ];         // dt_i exp(r_I - cs_i)                          (off-diagonal blocks)
     float dg[kQ];        // dt_i exp(r_{I-1} - cs_i) if block I has a small span, else dt_i
@@ -96,8 +98,15 @@ __global__ __launch_bounds__(256, 3) void fp16_scan_kernel(
   {
     const __amdgpu_buffer_rsrc_t xrs = buffer_rsrc(x + tok0 * HP + (size_t)h * kP);
     const uint32_t xo = (uint32_t)((jb * 32 * HP + p0) * sizeof(XT));
+    // x and y streamed when they exceed the Infinity Cache, as in the INT8 layer's scan
+    if (stream) {
 #pragma unroll
-    for (int r = 0; r < 32; ++r) xr[r] = Pair<XT>::load(xrs, xo, (uint32_t)(r * HP * sizeof(XT)));
+      for (int r = 0; r < 32; ++r)
+        xr[r] = Pair<XT>::template load<kPolicyNT>(xrs, xo, (uint32_t)(r * HP * sizeof(XT)));
+    } else {
+#pragma unroll
+      for (int r = 0; r < 32; ++r) xr[r] = Pair<XT>::load(xrs, xo, (uint32_t)(r * HP * sizeof(XT)));
+    }
   }
 
   float dtv = dt[(tok0 + t) * H + h];
@@ -312,10 +321,17 @@ __global__ __launch_bounds__(256, 3) void fp16_scan_kernel(
       const uint8_t* src = s_y + jt8 * 128 + ((col ^ (jt8 & 7)) * 16);
       const __amdgpu_buffer_rsrc_t yrs = buffer_rsrc(y + tok0 * HP + (size_t)h * kP);
       const uint32_t yo = (uint32_t)(jt8 * HP * 2 + col * 16);
+      if (stream) {
 #pragma unroll
-      for (int k = 0; k < (kQ * kP * 2) / (16 * 256); ++k)
-        buf_store16(*reinterpret_cast<const uint4*>(src + k * 32 * 128), yrs, yo,
-                    (uint32_t)(k * 32 * HP * 2));
+        for (int k = 0; k < (kQ * kP * 2) / (16 * 256); ++k)
+          buf_store16<kPolicyNT>(*reinterpret_cast<const uint4*>(src + k * 32 * 128), yrs, yo,
+                                 (uint32_t)(k * 32 * HP * 2));
+      } else {
+#pragma unroll
+        for (int k = 0; k < (kQ * kP * 2) / (16 * 256); ++k)
+          buf_store16(*reinterpret_cast<const uint4*>(src + k * 32 * 128), yrs, yo,
+                      (uint32_t)(k * 32 * HP * 2));
+      }
     }
   }
 }
@@ -328,10 +344,11 @@ hipError_t launch_fp16_scan(const LayerDims& d, const void* x, int x_dtype, cons
                             int y_dtype, hipStream_t st) {
   const int64_t nwork = (int64_t)d.batch * d.nchunks * d.nheads;
   if (nwork == 0) return hipSuccess;
+  const int stream = stream_xy(d, x_dtype == 1 ? 2 : 4, y_dtype == 1 ? 2 : 4);
 #define SSDI8_F16SCAN_LAUNCH(XT, YT)                                                           \
   hipLaunchKernelGGL((fp16_scan_kernel<XT, YT>), dim3((unsigned)nwork), dim3(256), 0, st,       \
                      static_cast<const XT*>(x), dt, A, c_frag, pin, cb, D, dt_softplus,        \
-                     static_cast<YT*>(y), d.seqlen, d.nheads, d.ngroups, d.nchunks)
+                     static_cast<YT*>(y), d.seqlen, d.nheads, d.ngroups, d.nchunks, stream)
   if (x_dtype == 1 && y_dtype == 1) SSDI8_F16SCAN_LAUNCH(_Float16, _Float16);
   else if (x_dtype == 1) SSDI8_F16SCAN_LAUNCH(_Float16, float);
   else if (y_dtype == 1) SSDI8_F16SCAN_LAUNCH(float, _Float16);

@@ -54,12 +54,13 @@ hipError_t launch_state_pass(int64_t batch, int64_t nchunks, int64_t nheads, int
                              int frag_k, hipStream_t st);
 
 // ChunkScan1 (int8) + ChunkScan2 (fp16) + output epilogue; C_q, P_in and CB_q in fragment order.
+// stream: x and y read / written non-temporally (stream_xy).
 hipError_t launch_chunk_scan(const LayerDims& d, const void* x, int x_dtype, const float* dt,
                              int dt_softplus, const float* A, const int8_t* cq_frag,
                              const float* C_scale, int c_per_token, const int8_t* pin,
                              const int8_t* cbq, const float* cb_scale, const float* state_scale,
                              const float* D, const float* corr, void* y, int y_dtype,
-                             int32_t* y1_tap, hipStream_t st);
+                             int32_t* y1_tap, int stream, hipStream_t st);
 
 // Single pass of ChunkState, StatePassing and ChunkScan (fp16 x): one workgroup per (b, c, h)
 // in ticket order; each computes its chunk's S_q, obtains P_in[c] from the chunks before it (the
@@ -98,7 +99,16 @@ struct FusedState {
   int nclass = 8;       // sync_classes(nbh)
   int spin_limit = 0;
   int speculate = 0;    // request the predicted item's first loads with its ticket (small grids)
+  int stream = 0;       // x and y non-temporal (stream_xy)
 };
+// Whether a layer's x and y (touched once by the scan kernels) are streamed through the caches
+// instead of cached: when together they exceed the 256 MB Infinity Cache, caching them only
+// displaces the tiles every head of a chunk re-reads; below it, they stay resident for whatever
+// reads them next.
+inline int stream_xy(const LayerDims& d, int x_bytes, int y_bytes) {
+  const int64_t elems = (int64_t)d.batch * d.seqlen * d.nheads * 64;   // P = 64
+  return elems * (x_bytes + y_bytes) > ((int64_t)256 << 20) ? 1 : 0;
+}
 hipError_t launch_chunk_scan_fused(const LayerDims& d, const _Float16* x, const float* dt,
                                    int dt_softplus, const float* A, const int8_t* cq_frag,
                                    const float* C_scale, int c_per_token, int8_t* pin,
