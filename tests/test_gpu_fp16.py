@@ -74,13 +74,16 @@ def test_fp16_initial_state_and_fp32_output(torch, ssdi8):
     _check_state(g["final_state"].cpu().numpy(), ref["final_state"], "final state")
 
 
-def test_fp16_full_size_sampled_slabs(torch, ssdi8):
-    cfg = synth.CONFIGS["mamba2-130m"]
+@pytest.mark.parametrize("name", ["mamba2-130m", "mamba2-2.7b"])
+def test_fp16_full_size_sampled_slabs(torch, ssdi8, name):
+    """Full-size layers, the 2.7B-shaped one with x and y streamed through the caches."""
+    cfg = synth.CONFIGS[name]
+    say(f"fp16 layer full size {name}")
     inp = synth.draw(cfg, 1)
     g = _run(torch, ssdi8, inp)
     y = g["y"].float().cpu().numpy()
     fin = g["final_state"].cpu().numpy()
-    picks = [(0, 0), (cfg.batch - 1, cfg.nheads - 1), (3, 11)]
+    picks = [(0, 0), (cfg.batch - 1, cfg.nheads - 1), (cfg.batch // 2, cfg.nheads // 2)]
     ref = ofp.ssd_fp16_forward(inp["x"], inp["dt_raw"], inp["A"], inp["B"], inp["C"], inp["D"],
                                chunk=cfg.chunk, heads=picks)
     for (b, h) in picks:
