@@ -478,13 +478,20 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
       int8_t* slab = slab_of(pin, c + 1);
       st_sc1(same ? sq0 : step(z, sq0, 0), slab, off0);
       st_sc1(same ? sq1 : step(z, sq1, 0), slab, off1);
-      __builtin_amdgcn_s_waitcnt(0);
-      __syncthreads();
+    }
+    // its flag, once every wave's stores are complete: for c > 0 together with the first look,
+    // whose flag loads are in flight meanwhile (one wait and one barrier for both)
+    auto publish_early = [&]() {
       if (t == 0)
         __hip_atomic_store(flags + c, (int)kFlagP, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
+    };
     uint4 p0, p1;   // P_in[c]
     if (c == 0) {
+      if (early) {
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+        publish_early();
+      }
       // the initial state (row-major; 0 without one), also ChunkScan1's entering state of chunk 0
       uint32_t w[2][4];
 #pragma unroll
@@ -507,7 +514,9 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
         if (lane == 0) sm.misc[2] = l;
         if (lane < kLook) sm.lq[lane] = (int)(f & 0xffffu);
       }
+      if (early) __builtin_amdgcn_s_waitcnt(0);
       __syncthreads();
+      if (early) publish_early();
       int l = __builtin_amdgcn_readfirstlane(sm.misc[2]);
       if (l < 0) {
         // publish S_q[c] for the chunks after this one (unless P_in[c+1] already is), then wait
