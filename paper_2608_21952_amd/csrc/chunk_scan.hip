@@ -485,7 +485,10 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
       if (t == 0)
         __hip_atomic_store(flags + c, (int)kFlagP, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     };
-    uint4 p0, p1;   // P_in[c]
+    uint4 p0 = make_uint4(0u, 0u, 0u, 0u), p1 = p0;   // P_in[c]
+    // an early chunk whose predecessor had published P_in[c] uses it only in ChunkScan1, which
+    // loads it itself: no state loads, no stores after the look, so no closing barrier
+    bool quiet = false;
     if (c == 0) {
       if (early) {
         __builtin_amdgcn_s_waitcnt(0);
@@ -551,33 +554,36 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
         __syncthreads();
         l = __builtin_amdgcn_readfirstlane(sm.misc[2]);
       }
+      quiet = early && l == 0;
       // P_in[c-l] (published by the anchor chunk c-1-l) and the S_q of chunks c-l .. c-1, all
       // loads in flight together
-      const int8_t* pslab = slab_of(pin, c - l);
-      p0 = ld_sc1(pslab, off0);
-      p1 = ld_sc1(pslab, off1);
-      uint4 s0[kLook - 1], s1[kLook - 1];
+      if (!quiet) {
+        const int8_t* pslab = slab_of(pin, c - l);
+        p0 = ld_sc1(pslab, off0);
+        p1 = ld_sc1(pslab, off1);
+        uint4 s0[kLook - 1], s1[kLook - 1];
 #pragma unroll
-      for (int k = 0; k < kLook - 1; ++k) {
-        if (k < l) {
-          const int8_t* sslab = slab_of(fs.sq, c - l + k);
-          s0[k] = ld_sc1(sslab, off0);
-          s1[k] = ld_sc1(sslab, off1);
+        for (int k = 0; k < kLook - 1; ++k) {
+          if (k < l) {
+            const int8_t* sslab = slab_of(fs.sq, c - l + k);
+            s0[k] = ld_sc1(sslab, off0);
+            s1[k] = ld_sc1(sslab, off1);
+          }
         }
-      }
 #pragma unroll
-      for (int k = 0; k < kLook - 1; ++k) {
-        if (k < l) {
-          const int qk = sm.lq[l - 1 - k];   // Q(Decay) of chunk c - l + k
-          p0 = step(p0, s0[k], qk);
-          p1 = step(p1, s1[k], qk);
+        for (int k = 0; k < kLook - 1; ++k) {
+          if (k < l) {
+            const int qk = sm.lq[l - 1 - k];   // Q(Decay) of chunk c - l + k
+            p0 = step(p0, s0[k], qk);
+            p1 = step(p1, s1[k], qk);
+          }
         }
-      }
-      if (l > 0) {
-        // ChunkScan1 reads the entering state from the pin slot of this chunk
-        int8_t* slab = slab_of(pin, c);
-        st_sc1(p0, slab, off0);
-        st_sc1(p1, slab, off1);
+        if (l > 0) {
+          // ChunkScan1 reads the entering state from the pin slot of this chunk
+          int8_t* slab = slab_of(pin, c);
+          st_sc1(p0, slab, off0);
+          st_sc1(p1, slab, off1);
+        }
       }
     }
     // P_in[c+1] = clamp(S_q[c] + ((q_d P_in[c] + r) >> k))
@@ -604,8 +610,10 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
         }
       }
     }
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
+    if (!quiet) {
+      __builtin_amdgcn_s_waitcnt(0);
+      __syncthreads();
+    }
     if (t == 0 && c + 1 < nc && !early)
       __hip_atomic_store(flags + c, (int)(kFlagP | (uint32_t)qd), __ATOMIC_RELAXED,
                          __HIP_MEMORY_SCOPE_AGENT);
