@@ -1,7 +1,10 @@
 """Register and LDS budgets of the hot kernels, from the compiler's resource-usage remarks
-(gfx950, the library's own flags): no VGPR or SGPR spills (a spilled value's reload is a
-vector-memory load, which waits behind every load in flight), and the single pass and the
-separate ChunkScan within four workgroups per CU (at most 128 VGPRs, 40 KB of LDS)."""
+(gfx950, the library's own flags): no VGPR spills and no scratch memory at all (a value
+reloaded from scratch is a vector-memory load, which waits behind every load in flight), and
+the single pass and the separate ChunkScan within four workgroups per CU (at most 128 VGPRs,
+40 KB of LDS).  A few SGPRs may spill into the lanes of a VGPR (v_writelane / v_readlane, no
+memory access): the single pass's instantiations with fp16 output hold 4-6 that way, counted in
+their VGPRs."""
 import os
 import re
 import shutil
@@ -25,7 +28,7 @@ def _resources(src):
         if m:
             cur = out.setdefault(m.group(1), {})
             continue
-        m = re.search(r"remark:\s+([A-Za-z ]+?)(?: \[bytes/block\])?: (\d+)", line)
+        m = re.search(r"remark:\s+([A-Za-z ]+?)(?: \[bytes/(?:block|lane)\])?: (\d+)", line)
         if m and cur is not None:
             cur[m.group(1).strip()] = int(m.group(2))
     return out
@@ -42,7 +45,8 @@ def test_no_register_spills(src):
     assert res, f"no kernels found in {src}"
     for name, r in res.items():
         assert r.get("VGPRs Spill", 0) == 0, f"{name}: {r}"
-        assert r.get("SGPRs Spill", 0) == 0, f"{name}: {r}"
+        assert r["ScratchSize"] == 0, f"{name}: {r}"
+        assert r.get("SGPRs Spill", 0) <= 8, f"{name}: {r}"
 
 
 def test_chunk_scan_fits_four_workgroups_per_cu():
