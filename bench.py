@@ -467,8 +467,8 @@ def main():
     per_step = sorted(marks[k].elapsed_time(marks[k + 1]) for k in range(K))
     ms_median = per_step[K // 2] if K % 2 else 0.5 * (per_step[K // 2 - 1] + per_step[K // 2])
     if graph is not None:
-        # per-kernel durations: K eager steps right after, with HIP events recorded on the
-        # launch stream between the kernels (same kernels; an event record adds ~1-3 us)
+        # per-kernel durations: K eager steps right after, with the library's stage events
+        # (ChunkBMM and the scan kernel set theirs from their own dispatch: start and end)
         queue_ahead(torch, K)
         for k in range(K):
             step(k)
@@ -485,7 +485,7 @@ def main():
             per["quantize_B"] += ev.elapsed_ms(base, base + 1)
             per["quantize_C"] += ev.elapsed_ms(base + 1, base + 2)
         if single:
-            # events 1-3 are recorded back to back before the single pass
+            # stage events 0-1: ChunkBMM's start and end; 3-4: the single pass's
             per["chunk_bmm"] += ev.elapsed_ms(base + 2, base + 3)
             per["single_pass"] += ev.elapsed_ms(base + 5, base + 6)
         else:

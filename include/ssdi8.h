@@ -152,10 +152,13 @@ typedef struct {
   int8_t* cb_q;                       /* [B,c,G,Q,Q] C.B^T int8, entries i <= j only             */
   int32_t* scan1_i32;                 /* [B,L,H,P]   C_q . P_in^T int32 (ChunkScan1 product)     */
   void* workspace; size_t workspace_bytes;
-  /* Optional per-module timing: NULL, or 5 hipEvent_t handles created by the caller; they are
-     recorded on `stream` before ChunkBMM, before ChunkState, before StatePassing, before
-     ChunkScan and after ChunkScan (the module breakdown of the paper's latency figures).
-     Leave NULL when the call is captured into a HIP graph. */
+  /* Optional per-module timing: NULL, or 5 hipEvent_t handles created by the caller (with
+     timing enabled), marking the start of ChunkBMM, ChunkState, StatePassing and ChunkScan and
+     the end of ChunkScan (the module breakdown of the paper's latency figures).  Events 0 and 1
+     are set by ChunkBMM's own dispatch (its start and end), events 3 and 4 by the ChunkScan
+     kernel's (hipExtLaunchKernelGGL: the timestamps a profiler's kernel trace reports), event 2
+     is recorded on `stream` after ChunkState.  Leave NULL when the call is captured into a
+     HIP graph. */
   void* const* stage_events;
   /* Kernel path.  With fp16 x and none of the taps xs_q, state_i32, state_q, decay_q, scan1_i32,
      dt_post requested, ChunkState, StatePassing and ChunkScan can run as one single-pass kernel
@@ -166,7 +169,8 @@ typedef struct {
      takes enough concurrent sequences to hide the serial hand-offs: batch * nheads >= 72 with
      at least 4 chunks, or >= 48 with at least 32); 1: always the separate kernels; 2: the
      single pass whenever eligible.
-     With the single pass, events 1-3 of stage_events are recorded back to back before it. */
+     With the single pass, events 1-2 of stage_events mark the end of ChunkBMM and 3-4 the
+     single pass's own start and end. */
   int path;
   /* Alternative to Bq / Cq (both NULL then): the unquantized B, C [B,L,G,N] of bc_dtype
      (SSDI8_F16 or SSDI8_F32), quantized inside ChunkBMM with the static steps B_scale, C_scale

@@ -323,21 +323,25 @@ ssdi8_status ssdi8_ssd_chunk_scan(const ssdi8_dims* d, const ssdi8_scan_args* a,
   int8_t* cbq = reinterpret_cast<int8_t*>(ws + plan.cbq);
   int16_t* qd = a->decay_q ? a->decay_q : reinterpret_cast<int16_t*>(ws + plan.qd);
 
+  // stage events: 0 and 1 are ChunkBMM's own start and end, 3 and 4 the ChunkScan (or single
+  // pass) kernel's; 2 is recorded on the stream after ChunkState (after ChunkBMM on the single
+  // pass), so StatePassing's share runs from it to ChunkScan's start
+  hipEvent_t ev[5] = {};
+  if (a->stage_events)
+    for (int i = 0; i < 5; ++i) ev[i] = static_cast<hipEvent_t>(a->stage_events[i]);
   auto mark = [&](int i) -> bool {
-    return !a->stage_events ||
-           hipEventRecord(static_cast<hipEvent_t>(a->stage_events[i]), st) == hipSuccess;
+    return !a->stage_events || hipEventRecord(ev[i], st) == hipSuccess;
   };
   const bool fused = single_pass(d, a);
   int* sync = reinterpret_cast<int*>(ws + plan.sync);
-  if (!mark(0)) return SSDI8_ERR_HIP;
   hipError_t e = ssdi8::launch_chunk_bmm(ld, Csrc, Bsrc, quantized ? -1 : a->bc_dtype,
                                          a->C_scale, a->c_per_token,
                                          a->B_scale, a->cb_scale, cbq, a->cb_q, a->cb_i32, bqT,
                                          cq, fused ? 1 : 0, sync, fused ? (int)plan.nsync : 0,
-                                         a->hand_off_timeouts, st);
-  if (e != hipSuccess || !mark(1)) return SSDI8_ERR_HIP;
+                                         a->hand_off_timeouts, st, ev[0], ev[1]);
+  if (e != hipSuccess) return SSDI8_ERR_HIP;
   if (fused) {
-    if (!mark(2) || !mark(3)) return SSDI8_ERR_HIP;
+    if (!mark(2)) return SSDI8_ERR_HIP;
     ssdi8::FusedState fs;
     fs.bqT = bqT;
     fs.sq = sq;
@@ -362,8 +366,8 @@ ssdi8_status ssdi8_ssd_chunk_scan(const ssdi8_dims* d, const ssdi8_scan_args* a,
     e = ssdi8::launch_chunk_scan_fused(ld, static_cast<const _Float16*>(a->x), a->dt,
                                        a->dt_softplus, a->A, cq, a->C_scale, a->c_per_token, pin,
                                        cbq, a->cb_scale, a->state_scale, a->D, a->corr, a->y,
-                                       a->y_dtype, fs, st);
-    if (e != hipSuccess || !mark(4)) return SSDI8_ERR_HIP;
+                                       a->y_dtype, fs, st, ev[3], ev[4]);
+    if (e != hipSuccess) return SSDI8_ERR_HIP;
     if (a->state_in_q) {
       e = ssdi8::launch_pin_tap(pin, a->state_in_q, (int64_t)ld.batch * ld.nchunks * ld.nheads,
                                 st);
@@ -380,14 +384,14 @@ ssdi8_status ssdi8_ssd_chunk_scan(const ssdi8_dims* d, const ssdi8_scan_args* a,
                                a->decay_shift, a->shift_round, a->init_state_q, pin,
                                a->state_in_q, a->final_state_q, a->final_state, a->state_scale,
                                (int)d->dstate, st);
-  if (e != hipSuccess || !mark(3)) return SSDI8_ERR_HIP;
+  if (e != hipSuccess) return SSDI8_ERR_HIP;
   e = ssdi8::launch_chunk_scan(ld, a->x, a->x_dtype, a->dt, a->dt_softplus, a->A, cq,
                                a->C_scale, a->c_per_token, pin, cbq, a->cb_scale, a->state_scale,
                                a->D, a->corr, a->y, a->y_dtype, a->scan1_i32,
                                ssdi8::stream_xy(ld, a->x_dtype == SSDI8_F16 ? 2 : 4,
                                                 a->y_dtype == SSDI8_F16 ? 2 : 4),
-                               st);
-  if (e != hipSuccess || !mark(4)) return SSDI8_ERR_HIP;
+                               st, ev[3], ev[4]);
+  if (e != hipSuccess) return SSDI8_ERR_HIP;
   return SSDI8_OK;
 }
 

@@ -24,6 +24,8 @@
 // B and C may also arrive unquantized (fp16 / fp32) with static steps: each row is then quantized
 // as it is loaded (the B/C quantization of Eq. 1 fused into this kernel, which is the only reader
 // of the row-major B_q, C_q), with the arithmetic of ssdi8_quantize_act.
+#include <hip/hip_ext.h>
+
 #include "common.hpp"
 #include "frag.hpp"
 #include "launch.hpp"
@@ -271,21 +273,31 @@ hipError_t launch_chunk_bmm(const LayerDims& d, const void* C, const void* B, in
                             const float* C_scale, int c_per_token, const float* B_scale,
                             const float* cb_scale, int8_t* cbq_frag, int8_t* cbq_tap,
                             int32_t* cb32_tap, int8_t* bqT_frag, int8_t* cq_frag, int cq_perm,
-                            int* sync, int nsync, int* timeouts, hipStream_t st) {
+                            int* sync, int nsync, int* timeouts, hipStream_t st,
+                            hipEvent_t ev_start, hipEvent_t ev_stop) {
   const int64_t ncg = (int64_t)d.batch * d.nchunks * d.ngroups;
   // parts per chunk-group: enough workgroups to reach every CU on small layers
   const int S = ncg <= 128 ? 4 : (ncg <= 256 ? 2 : 1);
   const int64_t nwork = ncg * S;
   if (nwork == 0) return hipSuccess;
+#define SSDI8_BMM_ARGS(T)                                                                       \
+  static_cast<const T*>(C), static_cast<const T*>(B), C_scale, c_per_token, B_scale, cb_scale,  \
+      cbq_frag, cbq_tap, cb32_tap, bqT_frag, cq_frag, cq_perm, sync, nsync, timeouts, d.seqlen, \
+      d.ngroups, d.nchunks, S
 #define SSDI8_BMM_LAUNCH(T)                                                                     \
-  hipLaunchKernelGGL(chunk_bmm_kernel<T>, dim3((unsigned)nwork), dim3(kThreads), 0, st,        \
-                     static_cast<const T*>(C), static_cast<const T*>(B), C_scale, c_per_token,  \
-                     B_scale, cb_scale, cbq_frag, cbq_tap, cb32_tap, bqT_frag, cq_frag,         \
-                     cq_perm, sync, nsync, timeouts, d.seqlen, d.ngroups, d.nchunks, S)
+  do {                                                                                          \
+    if (ev_start || ev_stop)                                                                    \
+      hipExtLaunchKernelGGL(chunk_bmm_kernel<T>, dim3((unsigned)nwork), dim3(kThreads), 0, st, \
+                            ev_start, ev_stop, 0, SSDI8_BMM_ARGS(T));                           \
+    else                                                                                        \
+      hipLaunchKernelGGL(chunk_bmm_kernel<T>, dim3((unsigned)nwork), dim3(kThreads), 0, st,    \
+                         SSDI8_BMM_ARGS(T));                                                    \
+  } while (0)
   if (src_dtype < 0) SSDI8_BMM_LAUNCH(int8_t);
   else if (src_dtype == 1) SSDI8_BMM_LAUNCH(_Float16);
   else SSDI8_BMM_LAUNCH(float);
 #undef SSDI8_BMM_LAUNCH
+#undef SSDI8_BMM_ARGS
   return hipGetLastError();
 }
 

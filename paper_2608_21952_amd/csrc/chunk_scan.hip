@@ -25,6 +25,8 @@
 // 128-byte rows.  C_q, P_in and CB_q arrive in MFMA fragment order (frag.hpp), so every operand
 // load is one contiguous 1 KB run per wave.  Under 40 KB of LDS and at most 128 VGPRs per lane
 // let four workgroups share a CU.
+#include <hip/hip_ext.h>
+
 #include "common.hpp"
 #include "frag.hpp"
 #include "launch.hpp"
@@ -911,23 +913,32 @@ hipError_t launch_chunk_scan(const LayerDims& d, const void* x, int x_dtype, con
                              const float* C_scale, int c_per_token, const int8_t* pin,
                              const int8_t* cbq, const float* cb_scale, const float* state_scale,
                              const float* D, const float* corr, void* y, int y_dtype,
-                             int32_t* y1_tap, int stream, hipStream_t st) {
+                             int32_t* y1_tap, int stream, hipStream_t st,
+                             hipEvent_t ev_start, hipEvent_t ev_stop) {
   const int64_t nwork = (int64_t)d.batch * d.nchunks * d.nheads;
   if (nwork == 0) return hipSuccess;
   const dim3 grid((unsigned)nwork), block(256);
   FusedState fs;
   fs.stream = stream;
-#define SSDI8_SCAN_LAUNCH(XT, YT)                                                             \
-  hipLaunchKernelGGL((chunk_scan_kernel<XT, YT, 0>), grid, block, 0, st,                      \
-                     static_cast<const XT*>(x), dt, A, cq_frag, C_scale, c_per_token,         \
-                     const_cast<int8_t*>(pin), cbq, cb_scale, state_scale, D, corr,           \
-                     dt_softplus, static_cast<YT*>(y), y1_tap, d.seqlen, d.nheads, d.ngroups, \
-                     d.nchunks, fs)
+#define SSDI8_SCAN_ARGS(XT, YT)                                                                  \
+  static_cast<const XT*>(x), dt, A, cq_frag, C_scale, c_per_token, const_cast<int8_t*>(pin),    \
+      cbq, cb_scale, state_scale, D, corr, dt_softplus, static_cast<YT*>(y), y1_tap, d.seqlen,   \
+      d.nheads, d.ngroups, d.nchunks, fs
+#define SSDI8_SCAN_LAUNCH(XT, YT)                                                                \
+  do {                                                                                           \
+    if (ev_start || ev_stop)                                                                     \
+      hipExtLaunchKernelGGL((chunk_scan_kernel<XT, YT, 0>), grid, block, 0, st, ev_start,        \
+                            ev_stop, 0, SSDI8_SCAN_ARGS(XT, YT));                                \
+    else                                                                                         \
+      hipLaunchKernelGGL((chunk_scan_kernel<XT, YT, 0>), grid, block, 0, st,                     \
+                         SSDI8_SCAN_ARGS(XT, YT));                                               \
+  } while (0)
   if (x_dtype == 1 && y_dtype == 1) SSDI8_SCAN_LAUNCH(_Float16, _Float16);
   else if (x_dtype == 1) SSDI8_SCAN_LAUNCH(_Float16, float);
   else if (y_dtype == 1) SSDI8_SCAN_LAUNCH(float, _Float16);
   else SSDI8_SCAN_LAUNCH(float, float);
 #undef SSDI8_SCAN_LAUNCH
+#undef SSDI8_SCAN_ARGS
   return hipGetLastError();
 }
 
@@ -936,19 +947,29 @@ hipError_t launch_chunk_scan_fused(const LayerDims& d, const _Float16* x, const 
                                    const float* C_scale, int c_per_token, int8_t* pin,
                                    const int8_t* cbq, const float* cb_scale,
                                    const float* state_scale, const float* D, const float* corr,
-                                   void* y, int y_dtype, const FusedState& fs, hipStream_t st) {
+                                   void* y, int y_dtype, const FusedState& fs, hipStream_t st,
+                                   hipEvent_t ev_start, hipEvent_t ev_stop) {
   const int64_t nwork = (int64_t)d.batch * d.nchunks * d.nheads;
   if (nwork == 0) return hipSuccess;
   const dim3 grid((unsigned)nwork), block(256);
+#define SSDI8_FUSED_ARGS(YT)                                                                     \
+  x, dt, A, cq_frag, C_scale, c_per_token, pin, cbq, cb_scale, state_scale, D, corr, dt_softplus, \
+      static_cast<YT*>(y), nullptr, d.seqlen, d.nheads, d.ngroups, d.nchunks, fs
 #define SSDI8_FUSED_LAUNCH(YT, M)                                                                \
-  hipLaunchKernelGGL((chunk_scan_kernel<_Float16, YT, M>), grid, block, 0, st, x, dt, A, cq_frag, \
-                     C_scale, c_per_token, pin, cbq, cb_scale, state_scale, D, corr, dt_softplus, \
-                     static_cast<YT*>(y), nullptr, d.seqlen, d.nheads, d.ngroups, d.nchunks, fs)
+  do {                                                                                           \
+    if (ev_start || ev_stop)                                                                     \
+      hipExtLaunchKernelGGL((chunk_scan_kernel<_Float16, YT, M>), grid, block, 0, st, ev_start,  \
+                            ev_stop, 0, SSDI8_FUSED_ARGS(YT));                                   \
+    else                                                                                         \
+      hipLaunchKernelGGL((chunk_scan_kernel<_Float16, YT, M>), grid, block, 0, st,               \
+                         SSDI8_FUSED_ARGS(YT));                                                  \
+  } while (0)
   if (y_dtype == 1 && fs.speculate) SSDI8_FUSED_LAUNCH(_Float16, 2);
   else if (y_dtype == 1) SSDI8_FUSED_LAUNCH(_Float16, 1);
   else if (fs.speculate) SSDI8_FUSED_LAUNCH(float, 2);
   else SSDI8_FUSED_LAUNCH(float, 1);
 #undef SSDI8_FUSED_LAUNCH
+#undef SSDI8_FUSED_ARGS
   return hipGetLastError();
 }
 

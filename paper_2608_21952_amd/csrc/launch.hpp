@@ -7,6 +7,10 @@
 
 namespace ssdi8 {
 
+// ev_start / ev_stop of the launchers that take them: NULL, or events set to the kernel's own
+// start and end (hipExtLaunchKernelGGL: the dispatch's timestamps, the figures a profiler's
+// kernel trace reports) rather than markers recorded between kernels.
+
 // Sizes shared by the SSD-layer kernels (P = 64, N = 128, Q = 256 fixed).
 struct LayerDims {
   int batch, seqlen, nheads, ngroups, nchunks;
@@ -30,7 +34,8 @@ hipError_t launch_chunk_bmm(const LayerDims& d, const void* C, const void* B, in
                             const float* C_scale, int c_per_token, const float* B_scale,
                             const float* cb_scale, int8_t* cbq_frag, int8_t* cbq_tap,
                             int32_t* cb32_tap, int8_t* bqT_frag, int8_t* cq_frag, int cq_perm,
-                            int* sync, int nsync, int* timeouts, hipStream_t st);
+                            int* sync, int nsync, int* timeouts, hipStream_t st,
+                            hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr);
 
 // ChunkCumsum + reformulated ChunkState (Eq. 7-8) and Q(Decay) (Eq. 9).
 hipError_t launch_chunk_state(const LayerDims& d, const void* x, int x_dtype, const float* dt,
@@ -60,7 +65,8 @@ hipError_t launch_chunk_scan(const LayerDims& d, const void* x, int x_dtype, con
                              const float* C_scale, int c_per_token, const int8_t* pin,
                              const int8_t* cbq, const float* cb_scale, const float* state_scale,
                              const float* D, const float* corr, void* y, int y_dtype,
-                             int32_t* y1_tap, int stream, hipStream_t st);
+                             int32_t* y1_tap, int stream, hipStream_t st,
+                             hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr);
 
 // Single pass of ChunkState, StatePassing and ChunkScan (fp16 x): one workgroup per (b, c, h)
 // in ticket order; each computes its chunk's S_q, obtains P_in[c] from the chunks before it (the
@@ -114,7 +120,8 @@ hipError_t launch_chunk_scan_fused(const LayerDims& d, const _Float16* x, const 
                                    const float* C_scale, int c_per_token, int8_t* pin,
                                    const int8_t* cbq, const float* cb_scale,
                                    const float* state_scale, const float* D, const float* corr,
-                                   void* y, int y_dtype, const FusedState& fs, hipStream_t st);
+                                   void* y, int y_dtype, const FusedState& fs, hipStream_t st,
+                                   hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr);
 
 // One-token decode step on the persistent int8 state (a chunk of one token), in place.
 hipError_t launch_decode(int64_t batch, int64_t nheads, int64_t ngroups, const void* x,
