@@ -32,8 +32,18 @@ SOURCE = {"single_pass": "chunk_scan"}      # kernel -> source file of its HIP c
 KERNEL_HEADERS = ("common.hpp", "exact_sum.hpp", "frag.hpp", "launch.hpp")
 
 
+def _code_only(text: str) -> str:
+    """The source without its comments and blank space, so that a comment edit does not count
+    as a change of the kernel (none of these sources has // or /* inside a string literal)."""
+    import re
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", "", text)
+    return "\n".join(" ".join(line.split()) for line in text.splitlines() if line.strip())
+
+
 def kernel_source_sha256(kernel: str):
-    """sha256 over the kernel's .hip source followed by the shared headers (None if missing)."""
+    """sha256 over the code of the kernel's .hip source followed by the shared headers, comments
+    and blank space left out (None if one is missing)."""
     import hashlib
     csrc = os.path.join(ROOT, "paper_2608_21952_amd", "csrc")
     h = hashlib.sha256()
@@ -41,8 +51,8 @@ def kernel_source_sha256(kernel: str):
         path = os.path.join(csrc, name)
         if not os.path.exists(path):
             return None
-        with open(path, "rb") as f:
-            h.update(f.read())
+        with open(path, encoding="utf-8") as f:
+            h.update(_code_only(f.read()).encode())
     return h.hexdigest()
 
 

@@ -399,9 +399,10 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
   //      the same recurrence, hence the same integers as a chain of hand-offs from chunk to
   //      chunk, without waiting for each of them.  A chunk that finds no such anchor at its first
   //      look publishes its own S_q (so that later chunks can look past it), then polls until it
-  //      does; every chunk then publishes P_in[c+1].  Only earlier chunks of the same sequence
-  //      are waited for; they hold earlier tickets of the same counter, so each is running or
-  //      done, publishes its S_q before it waits, and chunk 0 waits for nothing.  Waits are
+  //      does; every chunk then publishes P_in[c+1] (a chunk with Q(Decay) = 0 does so before
+  //      its first look, see below).  Only earlier chunks of the same sequence are waited for;
+  //      they hold earlier tickets of the same counter, so each is running or done, publishes
+  //      its S_q or its P_in[m+1] before it waits, and chunk 0 waits for nothing.  Waits are
   //      bounded: one that runs out is counted (sync[kSyncWait] and the caller's counter) and the
   //      kernel still finishes.  Each lane updates its own 32 state bytes in registers; payloads
   //      are written and read at the agent's coherence point (sc1) and are complete before

@@ -432,3 +432,12 @@ def test_scan_unquantized_bc_arguments(ssdi8):
     assert call() == ssdi8.ERR_NULL
     a.C = A16 + 4
     assert call() == ssdi8.ERR_ALIGN
+
+
+def test_traffic_source_hash_ignores_comments_only():
+    """The stored HBM traffic of a kernel stays valid across comment edits, not code edits."""
+    import bench
+    code = "int f() { return 1; } // one\n/* two\n   lines */ int g;\n"
+    assert bench._code_only(code) == bench._code_only("int f() {  return 1; }\n\nint g;")
+    assert bench._code_only(code) != bench._code_only("int f() { return 2; }\nint g;")
+    assert bench.kernel_source_sha256("single_pass") is not None
