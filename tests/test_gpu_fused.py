@@ -194,6 +194,44 @@ def test_single_pass_repeats_and_graph_replays(torch, ssdi8):
         assert layer.hand_off_timeouts() == 0, f"replay {rep}: counter not cleared or a wait ran out"
 
 
+
+@pytest.mark.parametrize("name", ["mamba2-130m", "mamba2-2.7b", "mamba2-8b-g8", "long-64k"])
+def test_single_pass_full_size_replays_are_identical(torch, ssdi8, name):
+    """At the benchmark sizes, in the launch configuration the benchmark times (one captured
+    graph of ChunkBMM and the single pass, replayed back to back): every replay reproduces the
+    eager call's y and final int8 state bit for bit, and no wait runs out."""
+    cfg = synth.CONFIGS[name]
+    reps = 30
+    say(f"single pass full size {name}: {reps} graph replays against the eager call")
+    inp = synth.draw(cfg, 1)
+    sc = calibration(cfg)
+    x, dt = dev(inp["x"], torch), dev(inp["dt_raw"], torch)
+    Bf, Cf = dev(inp["B"], torch), dev(inp["C"], torch)
+    layer = ssdi8.SSDi8Layer(inp["A"], inp["D"], sc["corr"], sc, device="cuda")
+    y = torch.empty_like(x)
+    first = layer(x, dt, Bf, Cf, y=y)
+    torch.cuda.synchronize()
+    assert layer.hand_off_timeouts() == 0
+    y_ref, fq_ref = y.clone(), first["final_state_q"].clone()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        layer(x, dt, Bf, Cf, y=y)
+    torch.cuda.current_stream().wait_stream(side)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        out = layer(x, dt, Bf, Cf, y=y)
+    for rep in range(reps):
+        y.zero_()
+        out["final_state_q"].zero_()
+        layer.timeouts.fill_(-1)
+        g.replay()
+        torch.cuda.synchronize()
+        assert layer.hand_off_timeouts() == 0, f"replay {rep}: a wait ran out"
+        assert torch.equal(y, y_ref), f"replay {rep}: y differs from the eager call"
+        assert torch.equal(out["final_state_q"], fq_ref), f"replay {rep}: final_q differs"
+    del y, y_ref, x
+
 def _fp16_overflow_matches_oracle(y16, y64, what):
     """Where the oracle's fp64 output rounds beyond the fp16 range (|y| >= 65520) the fp16
     output must be the infinity of the same sign, and finite elsewhere, except within the
