@@ -269,7 +269,9 @@ ssdi8_status ssdi8_decode_step(int64_t batch, int64_t nheads, int64_t headdim, i
  *     S = fp16(LUT_state·x)^T B,  P_in[c+1] = exp(cs_last) P_in[c] + S[c],
  *     y = (C · fp16(P_in)) exp(cs) + fp16(C B^T · dt · exp(segsum)) · x + D x
  * Sizes as ssdi8_ssd_chunk_scan; B and C are the unquantized fp16 (or fp32) tensors.  Scratch
- * goes through `workspace` (ssdi8_fp16_workspace_size); stage_events as in ssdi8_scan_args.
+ * goes through `workspace` (ssdi8_fp16_workspace_size).  stage_events: NULL or 5 hipEvent_t,
+ * all recorded on `stream` between the kernels: before ChunkBMM, ChunkState, StatePassing and
+ * ChunkScan and after ChunkScan.
  */
 typedef struct {
   const void* x; int x_dtype;         /* [B,L,H,P] fp16 or fp32                                   */
@@ -282,7 +284,7 @@ typedef struct {
   void* y; int y_dtype;               /* [B,L,H,P] output, fp16 or fp32                           */
   float* final_state;                 /* [B,H,P,N] fp32, or NULL                                  */
   void* workspace; size_t workspace_bytes;
-  void* const* stage_events;          /* NULL or 5 hipEvent_t (see ssdi8_scan_args)               */
+  void* const* stage_events;          /* NULL or 5 hipEvent_t (see above)                         */
 } ssdi8_fp16_args;
 size_t ssdi8_fp16_workspace_size(const ssdi8_dims* d);
 ssdi8_status ssdi8_ssd_chunk_scan_fp16(const ssdi8_dims* d, const ssdi8_fp16_args* a,
