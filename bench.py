@@ -212,11 +212,13 @@ def measured_peaks(torch, ssdi8):
                    "independent MFMA chains on register operands (ssdi8_mfma_probe)"}
 
 
-def queue_ahead(torch, K):
-    """Put a spin kernel of ~0.17 ms per step at the head of the stream, so that the host has
-    queued every eager launch of the K steps before the GPU reaches them: events between the
-    kernels then time GPU execution, not the host's launch latency."""
-    torch.cuda._sleep(int(400_000 * max(K, 1)))
+def keep_busy(graph, ms_step, seconds=0.05):
+    """Replay the captured step for about `seconds` of GPU time without waiting for it, so that
+    the host has queued the eager steps that follow before the GPU reaches them (it queues one
+    faster than the GPU runs one) and the GPU meanwhile runs real work at steady clocks (a spin
+    kernel would let them drop): events between those eager kernels then time GPU execution."""
+    for _ in range(max(1, int(seconds * 1e3 / max(ms_step, 1e-3)))):
+        graph.replay()
 
 
 def time_fp16(torch, ssdi8, cfg, x, dt, A, Bf, Cf, D, K, W):
@@ -251,7 +253,7 @@ def time_fp16(torch, ssdi8, cfg, x, dt, A, Bf, Cf, D, K, W):
     t1.record()
     torch.cuda.synchronize()
     ms = t0.elapsed_time(t1) / K
-    queue_ahead(torch, K)
+    keep_busy(graph, ms)
     for k in range(K):
         step(k)
     torch.cuda.synchronize()
@@ -479,7 +481,7 @@ def main():
     if graph is not None:
         # per-kernel durations: K eager steps right after, with the library's stage events
         # (ChunkBMM and the scan kernel set theirs from their own dispatch: start and end)
-        queue_ahead(torch, K)
+        keep_busy(graph, ms_step)
         for k in range(K):
             step(k)
         torch.cuda.synchronize()
@@ -546,7 +548,9 @@ def main():
                      "overhead_bytes": single_pass_overhead(cfg) if single else {},
                      "avg_us": round(per[dom] * 1e3, 2)},
         "timing": ("K replays of one captured HIP graph; per-kernel times from K eager steps "
-                   "bracketed by HIP events" if graph is not None else "eager launches"),
+                   "queued behind ~50 ms of replays, from the library's stage events (ChunkBMM "
+                   "and the scan kernel: their own dispatch start and end)"
+                   if graph is not None else "eager launches"),
         "settle": {"seconds": args.settle_s, "steps": settle_steps,
                    "what": "untimed steps after the warmup, until the GPU has run the layer "
                            "this long (clocks at steady state)"},
