@@ -109,8 +109,10 @@ __global__ __launch_bounds__(256, 4) void chunk_scan_kernel(
     int misc[4];         // single pass: ticket, q_d, look-back anchor
     int lq[kLook];       // single pass: Q(Decay) of chunks c-1, c-2, ... (flag words' low half)
     // x^T [p][i] fp16: the ChunkScan2 MFMA operand and, for fp16 x, the D skip operand; then
-    // the stage of the fp16 output (256 rows of 128 bytes).
-    uint8_t xT[kP * kXTS];
+    // the stage of the fp16 output (256 rows of 128 bytes).  16-byte aligned whatever the
+    // tables before it add up to: its 128-bit accesses split when it is not (a look-back depth
+    // that left it 4- or 8-byte aligned ran the single pass 34-55 % slower).
+    alignas(16) uint8_t xT[kP * kXTS];
   };
   __shared__ Smem sm;
   float2* s_u = sm.u;
