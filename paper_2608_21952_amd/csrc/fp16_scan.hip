@@ -72,7 +72,7 @@ __global__ __launch_bounds__(256, 3) void fp16_scan_kernel(
     float R[8][8];       // exp(r_a - r_b), b <= a
     double r[8];
     double scan[kScanScratch];
-    uint8_t xT[kP * kXTS];
+    alignas(16) uint8_t xT[kP * kXTS];   // 128-bit accesses: 16-byte aligned explicitly
   };
   __shared__ Smem sm;
   float* s_u = sm.u;
